@@ -1,0 +1,263 @@
+"""Throughput of the rdFFT + block-circulant hot path on one MI355X.
+
+One step is one pass of the whole hot path over one batch of synthetic input:
+  * the batched in-place transform workload, bf16 storage: for every n in
+    {64, 128, ..., 4096}, rdfft_forward then rdfft_inverse over 2^16 rows;
+  * the decoder-style block-circulant layer, bf16: d_in = d_out = 4096, p = 1024
+    (4 x 4 blocks), 8 x 512 = 4096 tokens, bca_forward then bca_backward
+    (including the dC token contraction).
+`value` is the algorithmic bytes of one step (each in-place row read once and
+written once; x, y, gy, dx, the spectra and dc once each) times the steps, over the
+wall time of the timed steps, in GB/s.  Inputs are resident in HBM before timing.
+Every buffer comes from a rotating pool of at least 1 GiB per workload so that no
+step is served from the 256 MB Infinity Cache.
+
+Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "rdFFT+BCA fwd/bwd GB/s (fraction of HBM peak), bf16; aux bytes = 0"
+HBM_PEAK_GBS = 8000.0
+NS = [64, 128, 256, 512, 1024, 2048, 4096]
+ROWS = 1 << 16
+BCA = dict(tokens=4096, d=4096, p=1024, sigma=0.01)
+POOL_BYTES = 1 << 30
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run one plain 1 GiB device copy (for HBM counter calibration)")
+    return ap.parse_args()
+
+
+def source_digest() -> str:
+    """Digest of the kernel sources, to tell whether stored counter readings are current."""
+    h = hashlib.sha256()
+    csrc = os.path.join(ROOT, "paper_2511_01385_amd", "csrc")
+    for name in sorted(os.listdir(csrc)):
+        if name.endswith((".hip", ".hpp", ".cpp", ".h")):
+            with open(os.path.join(csrc, name), "rb") as f:
+                h.update(name.encode() + f.read())
+    return h.hexdigest()[:16]
+
+
+def stored_traffic(kernel: str, digest: str):
+    path = os.path.join(PROFILE_DIR, "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        data = json.load(f)
+    rec = data.get(kernel)
+    if not rec or rec.get("source_digest") != digest:
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def cpu_baseline():
+    """The float64 NumPy oracle, untuned, on a bounded sample of the same workload."""
+    from oracle import bca as obca
+    from oracle import rdfft as ord_
+    from paper_2511_01385_amd import inputs
+
+    rows = 32768  # half the rows of every n
+    tokens = 2048  # half the layer tokens
+    d, p = BCA["d"], BCA["p"]
+    data = {n: inputs.to_f64(inputs.normal_rows(11 + n, rows, n, "bf16"), "bf16") for n in NS}
+    x, c, g = inputs.bca_problem(inputs.seed_for(4), tokens, d, d, p, BCA["sigma"], "bf16")
+    x, c, g = (inputs.to_f64(a, "bf16") for a in (x, c, g))
+    t0 = time.perf_counter()
+    for n in NS:
+        y = ord_.rdfft_forward(data[n])
+        ord_.rdfft_inverse(y)
+    obca.forward_spectral(x, c, d, p)
+    obca.backward_spectral(x, c, g, p)
+    dt = time.perf_counter() - t0
+    q = kb = d // p
+    nbytes = sum(4 * rows * n * 2 for n in NS)
+    nbytes += (2 * tokens * d * 2 + q * kb * p * 2) + (3 * tokens * d * 2 + q * kb * p * 2 + q * kb * p * 4)
+    return {
+        "value": round(nbytes / dt / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"float64 NumPy oracle (single-threaded) on half of one step: {rows} rows per n for "
+                  f"n={NS[0]}..{NS[-1]} forward+inverse, and the d=4096 p=1024 layer forward+backward on "
+                  f"{tokens} tokens; {dt:.1f} s",
+        "seconds": round(dt, 2),
+    }
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: --gpus {args.gpus} requested, but this build measures one GPU only "
+              "(rows and tokens would shard across GPUs with one dc all-reduce; see DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2511_01385_amd import api, inputs
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    api.rdfft_init()
+    stream = torch.cuda.current_stream()
+
+    def dev_bf16(stored):
+        return torch.from_numpy(np.ascontiguousarray(stored).view(np.int16)).view(torch.bfloat16).to(dev)
+
+    # --- inputs: one seeded buffer per workload, replicated into a >= 1 GiB pool
+    pools = {}
+    for n in NS:
+        base = dev_bf16(inputs.normal_rows(inputs.seed_for(2, salt=n), ROWS, n, "bf16"))
+        slots = max(2, -(-POOL_BYTES // (base.numel() * 2)))
+        pools[n] = [base] + [base.clone() for _ in range(slots - 1)]
+    T, d, p = BCA["tokens"], BCA["d"], BCA["p"]
+    q = kb = d // p
+    x, c, g = inputs.bca_problem(inputs.seed_for(4), T, d, d, p, BCA["sigma"], "bf16")
+    xb, cb, gb = dev_bf16(x), dev_bf16(c), dev_bf16(g)
+    set_bytes = 4 * T * d * 2
+    nsets = max(2, -(-POOL_BYTES // set_bytes))
+    sets = []
+    for _ in range(nsets):
+        sets.append(dict(x=xb.clone(), c=cb.clone(), g=gb.clone(), y=torch.empty_like(xb), dx=torch.empty_like(xb),
+                         dc=torch.empty((q, kb, p), dtype=torch.float32, device=dev)))
+    torch.cuda.synchronize()
+
+    calls = [(f"rdfft_forward_n{n}", n) for n in NS] + [(f"rdfft_inverse_n{n}", n) for n in NS]
+    bytes_of = {f"rdfft_forward_n{n}": 2 * ROWS * n * 2 for n in NS}
+    bytes_of.update({f"rdfft_inverse_n{n}": 2 * ROWS * n * 2 for n in NS})
+    bytes_of["bca_forward"] = 2 * T * d * 2 + q * kb * p * 2
+    bytes_of["bca_backward"] = 3 * T * d * 2 + q * kb * p * 2 + q * kb * p * 4
+    step_bytes = sum(bytes_of.values())
+    order = []
+    for n in NS:
+        order += [f"rdfft_forward_n{n}", f"rdfft_inverse_n{n}"]
+    order += ["bca_forward", "bca_backward"]
+
+    def run_step(i, events=None):
+        for n in NS:
+            buf = pools[n][i % len(pools[n])]
+            for name, fn in ((f"rdfft_forward_n{n}", api.rdfft_forward), (f"rdfft_inverse_n{n}", api.rdfft_inverse)):
+                if events is not None:
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    fn(buf)
+                    e1.record(stream)
+                    events[name].append((e0, e1))
+                else:
+                    fn(buf)
+        s = sets[i % len(sets)]
+        for name in ("bca_forward", "bca_backward"):
+            e0 = e1 = None
+            if events is not None:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            if name == "bca_forward":
+                api.bca_forward(s["x"], s["c"], s["y"])
+            else:
+                api.bca_backward(s["x"], s["c"], s["g"], s["dx"], s["dc"])
+            if events is not None:
+                e1.record(stream)
+                events[name].append((e0, e1))
+
+    for i in range(args.warmup):
+        run_step(i)
+    torch.cuda.synchronize()
+    if args.copy_calibration:
+        a = torch.empty(POOL_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+    alloc0 = torch.cuda.memory_allocated()
+    free0 = torch.cuda.mem_get_info()[0]
+    events = {name: [] for name in order}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        run_step(args.warmup + i, events)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    aux = (torch.cuda.memory_allocated() - alloc0) + (free0 - torch.cuda.mem_get_info()[0])
+
+    per_call = {}
+    for name in order:
+        us = [e0.elapsed_time(e1) * 1e3 for e0, e1 in events[name]]
+        avg = float(np.mean(us))
+        per_call[name] = {"avg_us": round(avg, 2), "GB_s": round(bytes_of[name] / avg / 1e3, 1),
+                          "bytes": bytes_of[name]}
+    dominant = max(order, key=lambda k: per_call[k]["avg_us"])
+    dom = per_call[dominant]
+    digest = source_digest()
+    kernel_name = {"bca_forward": "bca_forward_kernel", "bca_backward": "bca_backward_kernel"}.get(dominant, dominant)
+    roofline = {
+        "kernel": kernel_name,
+        "bound": "hbm",
+        "achieved": dom["GB_s"],
+        "peak": HBM_PEAK_GBS,
+        "unit": "GB/s",
+        "frac": round(dom["GB_s"] / HBM_PEAK_GBS, 4),
+        "traffic": stored_traffic(dominant, digest),
+        "avg_us": dom["avg_us"],
+        "algorithmic_bytes_per_launch": dom["bytes"],
+    }
+    value = step_bytes * args.steps / wall / 1e9
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "rdFFT+irdFFT bf16, 2^16 rows for each n in 64..4096, plus block-circulant layer bf16 "
+                        "d=4096 p=1024 (4x4 blocks) 4096 tokens forward+backward",
+            "rows": ROWS,
+            "n": NS,
+            "bca": {"d_in": d, "d_out": d, "p": p, "tokens": T},
+            "bytes_per_step": step_bytes,
+        },
+        "hbm_fraction": round(value / HBM_PEAK_GBS, 4),
+        "aux_bytes": int(aux),
+        "table_bytes": api.rdfft_table_bytes(),
+        "roofline": roofline,
+        "per_call": per_call,
+        "source_digest": digest,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

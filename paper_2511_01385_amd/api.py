@@ -1,0 +1,99 @@
+"""PyTorch-facing binding of the C ABI (same names as include/rdfft.h).
+
+Torch supplies device memory and the current stream; every call passes raw
+pointers and sizes to ``librdfft.so`` and checks the returned status.  No torch
+operation touches the data.
+"""
+
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib
+
+
+class RdfftError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {_lib.status_string(status)}")
+        self.status = status
+
+
+def _code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return _lib.RDFFT_F32
+    if t.dtype == torch.bfloat16:
+        return _lib.RDFFT_BF16
+    raise TypeError(f"rdfft supports float32 and bfloat16 storage, got {t.dtype}")
+
+
+def _dev(t: torch.Tensor, name: str) -> int:
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(t: torch.Tensor) -> int:
+    return torch.cuda.current_stream(t.device).cuda_stream
+
+
+def _check(status: int, what: str) -> None:
+    if status != _lib.RDFFT_OK:
+        raise RdfftError(status, what)
+
+
+def rdfft_forward(buf: torch.Tensor) -> torch.Tensor:
+    """In place: each row (last dim n) becomes its packed spectrum.  Returns ``buf``."""
+    n = buf.shape[-1]
+    rows = buf.numel() // n if n else 0
+    _check(_lib.load().rdfft_forward(_dev(buf, "buf"), rows, n, _code(buf), _stream(buf)), "rdfft_forward")
+    return buf
+
+
+def rdfft_inverse(buf: torch.Tensor) -> torch.Tensor:
+    """In place: each packed spectrum row becomes its real signal.  Returns ``buf``."""
+    n = buf.shape[-1]
+    rows = buf.numel() // n if n else 0
+    _check(_lib.load().rdfft_inverse(_dev(buf, "buf"), rows, n, _code(buf), _stream(buf)), "rdfft_inverse")
+    return buf
+
+
+def bca_forward(x: torch.Tensor, c_spectra: torch.Tensor, y: torch.Tensor) -> torch.Tensor:
+    """y[t] = W x[t] for the block-circulant W whose packed block spectra are ``c_spectra`` (q, kb, p)."""
+    q, kb, p = c_spectra.shape
+    tokens = x.shape[0]
+    st = _lib.load().bca_forward(
+        _dev(x, "x"), _dev(c_spectra, "c_spectra"), _dev(y, "y"), None,
+        kb * p, q * p, p, tokens, _code(x), _stream(x),
+    )
+    _check(st, "bca_forward")
+    return y
+
+
+def bca_backward(x: torch.Tensor, c_spectra: torch.Tensor, gy: torch.Tensor, dx: torch.Tensor, dc: torch.Tensor):
+    """Writes dL/dx into ``dx`` and dL/dc (float32, time domain, shape (q, kb, p)) into ``dc``.
+
+    ``gy`` is left unspecified; ``dx`` may be ``gy`` itself when d_in == d_out.
+    """
+    q, kb, p = c_spectra.shape
+    tokens = x.shape[0]
+    if dc.dtype != torch.float32:
+        raise TypeError("dc is float32")
+    grads = _lib.BcaGrads(_dev(dx, "dx"), _dev(dc, "dc"))
+    st = _lib.load().bca_backward(
+        _dev(x, "x"), _dev(c_spectra, "c_spectra"), _dev(gy, "gy"), ctypes.byref(grads),
+        kb * p, q * p, p, tokens, _code(x), _stream(x),
+    )
+    _check(st, "bca_backward")
+    return dx, dc
+
+
+def rdfft_init() -> None:
+    _check(_lib.load().rdfft_init(), "rdfft_init")
+
+
+def rdfft_table_bytes() -> int:
+    return int(_lib.load().rdfft_table_bytes())

@@ -1,0 +1,221 @@
+// capi.cpp -- the library's extern "C" entry points (declared in include/rdfft.h).
+//
+// Every entry point validates its arguments on the host before making any HIP call,
+// then enqueues its kernels on the caller's stream.  Nothing here allocates device
+// memory; the per-device twiddle table is a static __device__ array filled on first
+// use.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <atomic>
+#include <mutex>
+#include <vector>
+
+#include "launch.hpp"
+#include "plan.hpp"
+#include "rdfft.h"
+#include "twiddles.hpp"
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+
+struct DeviceState {
+  std::atomic<const float2*> tw{nullptr};
+  int num_cu = 0;
+};
+
+DeviceState g_dev[kMaxDevices];
+std::mutex g_init_mu;
+
+bool is_pow2(int64_t v) { return v > 0 && (v & (v - 1)) == 0; }
+
+int ilog2(int64_t v) {
+  int l = 0;
+  while ((int64_t(1) << l) < v) ++l;
+  return l;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// [a, a+na) and [b, b+nb) share a byte
+bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
+}
+
+int elem_bytes(int dtype) { return dtype == RDFFT_BF16 ? 2 : 4; }
+
+// products of sizes that must not overflow int64
+bool mul_ok(int64_t a, int64_t b, int64_t* out) {
+  if (a < 0 || b < 0) return false;
+  if (a != 0 && b > INT64_MAX / a) return false;
+  *out = a * b;
+  return true;
+}
+
+int ensure_device(const float2** tw, int* num_cu) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return RDFFT_EDEVICE;
+  DeviceState& st = g_dev[dev];
+  const float2* p = st.tw.load(std::memory_order_acquire);
+  if (p == nullptr) {
+    std::lock_guard<std::mutex> lock(g_init_mu);
+    p = st.tw.load(std::memory_order_relaxed);
+    if (p == nullptr) {
+      hipDeviceProp_t prop;
+      if (hipGetDeviceProperties(&prop, dev) != hipSuccess) return RDFFT_EDEVICE;
+      if (strncmp(prop.gcnArchName, "gfx950", 6) != 0) return RDFFT_EDEVICE;
+      static const std::vector<rdfft::HostC32> host = rdfft::build_twiddle_table();
+      if (rdfft::upload_twiddles(host.data(), host.size() * sizeof(rdfft::HostC32), &p) != hipSuccess)
+        return RDFFT_EDEVICE;
+      st.num_cu = prop.multiProcessorCount;
+      st.tw.store(p, std::memory_order_release);
+    }
+  }
+  *tw = p;
+  if (num_cu) *num_cu = st.num_cu;
+  return RDFFT_OK;
+}
+
+int check_transform(const void* buf, int64_t rows, int64_t n, int dtype) {
+  if (dtype != RDFFT_F32 && dtype != RDFFT_BF16) return RDFFT_EINVAL;
+  if (rows < 0) return RDFFT_EINVAL;
+  if (n < 2 || (n & 1)) return RDFFT_EINVAL;
+  if (!is_pow2(n) || n > (int64_t(2) << rdfft::kMaxLogN)) return RDFFT_EUNSUPPORTED;
+  if (rows == 0) return RDFFT_OK;
+  int64_t count = 0, bytes = 0;
+  if (!mul_ok(rows, n, &count) || !mul_ok(count, elem_bytes(dtype), &bytes)) return RDFFT_EINVAL;
+  if (buf == nullptr || !aligned16(buf)) return RDFFT_EINVAL;
+  return RDFFT_OK;
+}
+
+int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream, bool inv) {
+  int st = check_transform(buf, rows, n, dtype);
+  if (st != RDFFT_OK || rows == 0) return st;
+  const float2* tw = nullptr;
+  st = ensure_device(&tw, nullptr);
+  if (st != RDFFT_OK) return st;
+  const hipError_t e = rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype == RDFFT_BF16, inv, tw,
+                                                reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
+}
+
+struct BcaShape {
+  int q = 0, kb = 0, logp = 0;
+  int64_t x_bytes = 0, y_bytes = 0, c_bytes = 0, dc_bytes = 0;
+};
+
+int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t d_out, int64_t p, int64_t tokens,
+              int dtype, BcaShape* sh) {
+  if (dtype != RDFFT_F32 && dtype != RDFFT_BF16) return RDFFT_EINVAL;
+  if (tokens < 0 || d_in <= 0 || d_out <= 0 || p <= 0) return RDFFT_EINVAL;
+  if (p < 2 || (p & 1)) return RDFFT_EINVAL;
+  if (d_in % p != 0 || d_out % p != 0) return RDFFT_EINVAL;
+  if (!is_pow2(p)) return RDFFT_EUNSUPPORTED;
+  const int64_t q = d_out / p, kb = d_in / p;
+  if (q > (1 << 20) || kb > (1 << 20)) return RDFFT_EUNSUPPORTED;
+  sh->q = (int)q;
+  sh->kb = (int)kb;
+  sh->logp = ilog2(p);
+  if (!rdfft::bca_shape_supported(sh->logp, sh->q, sh->kb)) return RDFFT_EUNSUPPORTED;
+  const int s = elem_bytes(dtype);
+  int64_t t = 0;
+  if (!mul_ok(tokens, d_in, &t) || !mul_ok(t, s, &sh->x_bytes)) return RDFFT_EINVAL;
+  if (!mul_ok(tokens, d_out, &t) || !mul_ok(t, s, &sh->y_bytes)) return RDFFT_EINVAL;
+  if (!mul_ok(q * kb, p, &t) || !mul_ok(t, s, &sh->c_bytes)) return RDFFT_EINVAL;
+  sh->dc_bytes = t * 4;
+  if (c == nullptr || !aligned16(c)) return RDFFT_EINVAL;
+  if (tokens > 0) {
+    if (x == nullptr || y == nullptr || !aligned16(x) || !aligned16(y)) return RDFFT_EINVAL;
+    if (overlaps(c, sh->c_bytes, x, sh->x_bytes) || overlaps(c, sh->c_bytes, y, sh->y_bytes)) return RDFFT_EINVAL;
+  }
+  return RDFFT_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int rdfft_forward(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+  return transform(buf, rows, n, dtype, stream, false);
+}
+
+int rdfft_inverse(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+  return transform(buf, rows, n, dtype, stream, true);
+}
+
+int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grads, int64_t d_in, int64_t d_out,
+                int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream) {
+  if (grads != nullptr) return RDFFT_EINVAL;
+  BcaShape sh;
+  int st = check_bca(x, c_spectra, y, d_in, d_out, p, tokens, dtype, &sh);
+  if (st != RDFFT_OK) return st;
+  if (tokens == 0) return RDFFT_OK;
+  // y may be x itself (an in-place layer) only when the shapes agree
+  if (y == x) {
+    if (d_in != d_out) return RDFFT_EINVAL;
+  } else if (overlaps(x, sh.x_bytes, y, sh.y_bytes)) {
+    return RDFFT_EINVAL;
+  }
+  const float2* tw = nullptr;
+  st = ensure_device(&tw, nullptr);
+  if (st != RDFFT_OK) return st;
+  rdfft::BcaArgs a{x, c_spectra, y, nullptr, nullptr, tokens, sh.q, sh.kb, sh.logp, dtype == RDFFT_BF16};
+  return rdfft::launch_bca_forward(a, tw, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? RDFFT_OK
+                                                                                               : RDFFT_ELAUNCH;
+}
+
+int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* grads, int64_t d_in, int64_t d_out,
+                 int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream) {
+  if (grads == nullptr) return RDFFT_EINVAL;
+  BcaShape sh;
+  int st = check_bca(x, c_spectra, gy, d_in, d_out, p, tokens, dtype, &sh);
+  if (st != RDFFT_OK) return st;
+  float* dc = grads->dc;
+  void* dx = grads->dx;
+  if (dc == nullptr || !aligned16(dc)) return RDFFT_EINVAL;
+  if (overlaps(dc, sh.dc_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
+  if (tokens > 0) {
+    if (dx == nullptr || !aligned16(dx)) return RDFFT_EINVAL;
+    if (overlaps(x, sh.x_bytes, gy, sh.y_bytes)) return RDFFT_EINVAL;
+    if (overlaps(dx, sh.x_bytes, x, sh.x_bytes) || overlaps(dx, sh.x_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
+    if (dx == gy) {
+      if (d_in != d_out) return RDFFT_EINVAL;
+    } else if (overlaps(dx, sh.x_bytes, gy, sh.y_bytes)) {
+      return RDFFT_EINVAL;
+    }
+    if (overlaps(dc, sh.dc_bytes, x, sh.x_bytes) || overlaps(dc, sh.dc_bytes, gy, sh.y_bytes) ||
+        overlaps(dc, sh.dc_bytes, dx, sh.x_bytes))
+      return RDFFT_EINVAL;
+  }
+  const float2* tw = nullptr;
+  int num_cu = 0;
+  st = ensure_device(&tw, &num_cu);
+  if (st != RDFFT_OK) return st;
+  rdfft::BcaArgs a{x, c_spectra, gy, dx, dc, tokens, sh.q, sh.kb, sh.logp, dtype == RDFFT_BF16};
+  return rdfft::launch_bca_backward(a, tw, reinterpret_cast<hipStream_t>(stream), num_cu) == hipSuccess
+             ? RDFFT_OK
+             : RDFFT_ELAUNCH;
+}
+
+int rdfft_init(void) {
+  const float2* tw = nullptr;
+  return ensure_device(&tw, nullptr);
+}
+
+int64_t rdfft_table_bytes(void) { return (int64_t)rdfft::kTableEntries * 8; }
+
+const char* rdfft_status_string(int status) {
+  switch (status) {
+    case RDFFT_OK: return "RDFFT_OK";
+    case RDFFT_EINVAL: return "RDFFT_EINVAL: invalid argument";
+    case RDFFT_EUNSUPPORTED: return "RDFFT_EUNSUPPORTED: valid but unsupported size";
+    case RDFFT_ELAUNCH: return "RDFFT_ELAUNCH: HIP kernel launch failed";
+    case RDFFT_EDEVICE: return "RDFFT_EDEVICE: no usable gfx950 device or table upload failed";
+    default: return "unknown rdfft status";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,490 @@
+// fft_device.hpp -- device building blocks of the row transforms (gfx950, wave64).
+//
+// One row of n = 2N reals is transformed by TPR cooperating threads that each hold
+// E complex values in registers.  The N-point complex DFT of z_m = x_{2m} + i x_{2m+1}
+// runs as a Stockham sequence of radix-R passes (plan.hpp): every pass is a set of
+// register-resident radix-R DFTs preceded by twiddle multiplies; consecutive passes
+// exchange data through the row's LDS region.  The real-signal spectrum then follows
+// from a post-pass that pairs bins k and N-k (Sec. 4.1: the output of a real FFT is
+// conjugate-symmetric, so the n/2+1 bins Y_0..Y_{n/2} are squeezed into n reals).
+//
+// Packed ("pairs") layout of the result, as complex pair slots P[0..N-1]:
+//   P[0] = (Y_0, Y_{n/2}),  P[k] = Y_k for 1 <= k < N.
+//
+// The inverse runs the pre-pass (the algebraic inverse of the post-pass, with the
+// 1/n scale folded in) and the same passes with conjugated twiddles.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <type_traits>
+#include <utility>
+
+#include "plan.hpp"
+
+namespace rdfft {
+
+// ----------------------------------------------------------------------------------
+// compile-time loops
+template <class F, int... Is>
+__device__ __forceinline__ void static_for_impl(F&& f, std::integer_sequence<int, Is...>) {
+  (f(std::integral_constant<int, Is>{}), ...);
+}
+template <int N, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+  static_for_impl(f, std::make_integer_sequence<int, N>{});
+}
+
+// ----------------------------------------------------------------------------------
+// complex arithmetic on float2
+__device__ __forceinline__ float2 c_add(float2 a, float2 b) { return make_float2(a.x + b.x, a.y + b.y); }
+__device__ __forceinline__ float2 c_sub(float2 a, float2 b) { return make_float2(a.x - b.x, a.y - b.y); }
+__device__ __forceinline__ float2 c_conj(float2 a) { return make_float2(a.x, -a.y); }
+__device__ __forceinline__ float2 c_scale(float2 a, float s) { return make_float2(a.x * s, a.y * s); }
+
+// a * w, or a * conj(w) when CONJ
+template <bool CONJ>
+__device__ __forceinline__ float2 c_mul(float2 a, float2 w) {
+  if constexpr (!CONJ) return make_float2(fmaf(a.x, w.x, -a.y * w.y), fmaf(a.x, w.y, a.y * w.x));
+  else return make_float2(fmaf(a.x, w.x, a.y * w.y), fmaf(a.y, w.x, -a.x * w.y));
+}
+
+// cos(2 pi m / 32), m in [0, 8]; the rest follows by symmetry
+constexpr double kCos32[9] = {1.0,
+                              0.98078528040323044912618223613424,
+                              0.92387953251128675612818318939679,
+                              0.83146961230254523707878837761791,
+                              0.70710678118654752440084436210485,
+                              0.55557023301960222474283081394853,
+                              0.38268343236508977172845998403040,
+                              0.19509032201612826784828486847702,
+                              0.0};
+constexpr double cos32(int m) {
+  m &= 31;
+  return m <= 8 ? kCos32[m] : m <= 16 ? -kCos32[16 - m] : m <= 24 ? -kCos32[m - 16] : kCos32[32 - m];
+}
+constexpr double sin32(int m) { return cos32(m - 8); }
+
+// a * exp(-+ 2 pi i J / R): forward sign unless INV.  R divides 32.
+template <int R, int J, bool INV>
+__device__ __forceinline__ float2 rot(float2 a) {
+  constexpr int j = ((J % R) + R) % R;
+  if constexpr (j == 0) {
+    return a;
+  } else if constexpr (2 * j == R) {
+    return make_float2(-a.x, -a.y);
+  } else if constexpr (4 * j == R) {
+    return INV ? make_float2(-a.y, a.x) : make_float2(a.y, -a.x);
+  } else if constexpr (4 * j == 3 * R) {
+    return INV ? make_float2(a.y, -a.x) : make_float2(-a.y, a.x);
+  } else {
+    static_assert(32 % R == 0, "constant rotations need R | 32");
+    constexpr float c = (float)cos32(j * (32 / R));
+    constexpr float s = (float)sin32(j * (32 / R));
+    if constexpr (!INV) return make_float2(fmaf(a.x, c, a.y * s), fmaf(a.y, c, -a.x * s));
+    else return make_float2(fmaf(a.x, c, -a.y * s), fmaf(a.y, c, a.x * s));
+  }
+}
+
+// ----------------------------------------------------------------------------------
+// In-register DFT of R points, natural order in and out:
+//   v[k] <- sum_j v[j] exp(-+ 2 pi i j k / R)
+template <int R, bool INV>
+struct Dft;
+
+template <bool INV>
+struct Dft<1, INV> {
+  __device__ __forceinline__ static void run(float2*) {}
+};
+
+template <bool INV>
+struct Dft<2, INV> {
+  __device__ __forceinline__ static void run(float2* v) {
+    const float2 a = v[0], b = v[1];
+    v[0] = c_add(a, b);
+    v[1] = c_sub(a, b);
+  }
+};
+
+template <bool INV>
+struct Dft<4, INV> {
+  __device__ __forceinline__ static void run(float2* v) {
+    const float2 a0 = c_add(v[0], v[2]), a1 = c_sub(v[0], v[2]);
+    const float2 a2 = c_add(v[1], v[3]), a3 = rot<4, 1, INV>(c_sub(v[1], v[3]));
+    v[0] = c_add(a0, a2);
+    v[2] = c_sub(a0, a2);
+    v[1] = c_add(a1, a3);
+    v[3] = c_sub(a1, a3);
+  }
+};
+
+// R = R1 * R2 by one decimation-in-time step: n = R2*n1 + n2, k = k1 + R1*k2.
+template <int R1, int R2, bool INV>
+__device__ __forceinline__ void dft_split(float2* v) {
+  constexpr int R = R1 * R2;
+  float2 t[R];
+  static_for<R2>([&](auto n2c) {
+    constexpr int n2 = decltype(n2c)::value;
+    float2 u[R1];
+    static_for<R1>([&](auto n1c) { u[decltype(n1c)::value] = v[R2 * decltype(n1c)::value + n2]; });
+    Dft<R1, INV>::run(u);
+    static_for<R1>([&](auto k1c) {
+      constexpr int k1 = decltype(k1c)::value;
+      t[k1 * R2 + n2] = rot<R, n2 * k1, INV>(u[k1]);
+    });
+  });
+  static_for<R1>([&](auto k1c) {
+    constexpr int k1 = decltype(k1c)::value;
+    Dft<R2, INV>::run(&t[k1 * R2]);
+    static_for<R2>([&](auto k2c) {
+      constexpr int k2 = decltype(k2c)::value;
+      v[k1 + R1 * k2] = t[k1 * R2 + k2];
+    });
+  });
+}
+
+template <bool INV>
+struct Dft<8, INV> {
+  __device__ __forceinline__ static void run(float2* v) { dft_split<4, 2, INV>(v); }
+};
+template <bool INV>
+struct Dft<16, INV> {
+  __device__ __forceinline__ static void run(float2* v) { dft_split<4, 4, INV>(v); }
+};
+template <bool INV>
+struct Dft<32, INV> {
+  __device__ __forceinline__ static void run(float2* v) { dft_split<4, 8, INV>(v); }
+};
+
+// ----------------------------------------------------------------------------------
+// Row storage accessors (complex-pair indexed).
+struct GlobalF32 {
+  float2* base;
+  __device__ __forceinline__ float2 load(int m) const { return base[m]; }
+  __device__ __forceinline__ void store(int m, float2 v) const { base[m] = v; }
+};
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float2 bf16x2_to_f32(uint32_t u) {
+  return make_float2(__uint_as_float(u << 16), __uint_as_float(u & 0xffff0000u));
+}
+__device__ __forceinline__ uint32_t f32_to_bf16x2(float2 v) {  // round to nearest even
+  const f32x2_t f = {v.x, v.y};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
+}
+
+struct GlobalBF16 {
+  uint32_t* base;
+  __device__ __forceinline__ float2 load(int m) const { return bf16x2_to_f32(base[m]); }
+  __device__ __forceinline__ void store(int m, float2 v) const { base[m] = f32_to_bf16x2(v); }
+};
+
+// Read-only views (inputs that must never be written)
+struct ConstF32 {
+  const float2* base;
+  __device__ __forceinline__ float2 load(int m) const { return base[m]; }
+};
+struct ConstBF16 {
+  const uint32_t* base;
+  __device__ __forceinline__ float2 load(int m) const { return bf16x2_to_f32(base[m]); }
+};
+
+// A packed spectrum kept in a row's (padded) LDS region
+struct LdsSpectrum {
+  float2* base;
+  __device__ __forceinline__ float2 load(int m) const { return base[lds_pad(m)]; }
+  __device__ __forceinline__ void store(int m, float2 v) const { base[lds_pad(m)] = v; }
+};
+
+// ----------------------------------------------------------------------------------
+template <int LOGN>
+struct RowPlan {
+  static constexpr int N = 1 << LOGN;
+  static constexpr int NP = num_passes(LOGN);
+  static constexpr int E = kElems[LOGN];
+  static constexpr int C = kChunks[LOGN];
+  static constexpr int TPR = N / E;                       // threads per row
+  static constexpr int RW = TPR >= 256 ? 1 : 256 / TPR;   // rows per 256-thread workgroup
+  static constexpr int WG = TPR * RW;
+  // LDS float2 per row: one exchange chunk, or the half-spectrum partner exchange
+  static constexpr int LDS_F2 = TPR == 1 ? 0 : lds_padded_size(N / C > N / 2 ? N / C : N / 2);
+  static_assert(plan_is_consistent(LOGN), "inconsistent plan");
+  static_assert(C == 1 || E / radix(LOGN, 0) >= C, "chunked exchange needs >= C butterflies per thread");
+};
+
+// One Stockham pass q: twiddles (q > 0) then radix-R DFTs on the thread's butterflies.
+template <int LOGN, int Q, bool INV>
+__device__ __forceinline__ void stockham_compute(float2* v, int t, const float2* __restrict__ tw) {
+  using P = RowPlan<LOGN>;
+  constexpr int R = radix(LOGN, Q);
+  constexpr int Ns = stride_before(LOGN, Q);
+  constexpr int BPT = P::E / R;
+  if constexpr (Q > 0) {
+    const float2* __restrict__ twq = tw + pass_table_offset(LOGN, Q);
+    static_for<BPT>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int g = t + b * P::TPR;
+      const int k = g & (Ns - 1);
+      static_for<R - 1>([&](auto rc) {
+        constexpr int r = decltype(rc)::value + 1;
+        v[b * R + r] = c_mul<INV>(v[b * R + r], twq[(r - 1) * Ns + k]);
+      });
+    });
+  }
+  static_for<BPT>([&](auto bc) { Dft<R, INV>::run(&v[decltype(bc)::value * R]); });
+}
+
+// Exchange the outputs of pass Q into the inputs of pass Q+1 through LDS.
+// Pass Q writes out[(g/Ns)*Ns*R + (g mod Ns) + r*Ns]; pass Q+1 reads in[g + r*(N/R')].
+// With C chunks, round c moves the outputs whose destination lies in chunk c; for a
+// non-final pass that is decided by the butterfly index b, and for the reads by r.
+template <int LOGN, int Q>
+__device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds) {
+  using P = RowPlan<LOGN>;
+  constexpr int N = P::N, E = P::E, C = P::C, TPR = P::TPR;
+  constexpr int R = radix(LOGN, Q), Ns = stride_before(LOGN, Q), BPT = E / R;
+  constexpr int R2 = radix(LOGN, Q + 1), BPT2 = E / R2;
+  constexpr int CH = N / C;
+  static_assert(C == 1 || (BPT % C == 0 && R2 % C == 0), "chunking needs C | BPT and C | R'");
+  float2 nv[E];
+  static_for<C>([&](auto cc) {
+    constexpr int c = decltype(cc)::value;
+    static_for<BPT>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      if constexpr (b / (BPT / C) == c) {
+        const int g = t + b * TPR;
+        const int k = g & (Ns - 1);
+        const int base = (g - k) * R + k - c * CH;
+        static_for<R>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          lds[lds_pad(base + r * Ns)] = v[b * R + r];
+        });
+      }
+    });
+    __syncthreads();
+    static_for<BPT2>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int g = t + b * TPR;
+      static_for<R2>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        if constexpr (r / (R2 / C) == c) nv[b * R2 + r] = lds[lds_pad(g + r * (N / R2) - c * CH)];
+      });
+    });
+    __syncthreads();
+  });
+  static_for<E>([&](auto ic) { v[decltype(ic)::value] = nv[decltype(ic)::value]; });
+}
+
+template <int LOGN, int Q, bool INV>
+__device__ __forceinline__ void stockham_from(float2* v, int t, float2* lds, const float2* __restrict__ tw) {
+  stockham_compute<LOGN, Q, INV>(v, t, tw);
+  if constexpr (Q + 1 < RowPlan<LOGN>::NP) {
+    stockham_exchange<LOGN, Q>(v, t, lds);
+    stockham_from<LOGN, Q + 1, INV>(v, t, lds, tw);
+  }
+}
+
+// ----------------------------------------------------------------------------------
+// Forward rdFFT of one row.
+//   t      thread index within the row's TPR threads
+//   active false for padding rows past the end of the batch (no global access)
+//   src    input pairs (x_{2m}, x_{2m+1}), m < N
+//   dst    output packed pairs P[k]
+//   lds    the row's LDS region (RowPlan::LDS_F2 float2); may be the storage of dst
+//          when DST_IN_LDS (then a barrier separates the last LDS read from the stores)
+template <int LOGN, bool DST_IN_LDS, class Src, class Dst>
+__device__ __forceinline__ void row_forward(int t, bool active, const Src& src, const Dst& dst, float2* lds,
+                                            const float2* __restrict__ tw) {
+  using P = RowPlan<LOGN>;
+  constexpr int N = P::N, E = P::E, TPR = P::TPR;
+  if constexpr (LOGN == 0) {
+    // n = 2: Y_0 = x0 + x1, Y_1 = x0 - x1
+    if (active) {
+      const float2 z = src.load(0);
+      if constexpr (DST_IN_LDS) __syncthreads();
+      dst.store(0, make_float2(z.x + z.y, z.x - z.y));
+    } else if constexpr (DST_IN_LDS) {
+      __syncthreads();
+    }
+    return;
+  } else {
+    float2 v[E];
+    constexpr int R0 = radix(LOGN, 0), BPT0 = E / R0;
+    static_for<BPT0>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int g = t + b * TPR;
+      static_for<R0>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        v[b * R0 + r] = active ? src.load(g + r * (N / R0)) : make_float2(0.f, 0.f);
+      });
+    });
+    stockham_from<LOGN, 0, false>(v, t, lds, tw);
+
+    // Post-pass.  After the last pass thread t holds Z_m at m = g_b + r*(N/RL).
+    constexpr int RL = radix(LOGN, P::NP - 1), BPL = E / RL, NsL = N / RL;
+    const float2* __restrict__ twp = tw + post_table_offset(LOGN);
+    float2 partner[E / 2];
+    if constexpr (TPR == 1) {
+      // the whole row is in this thread's registers: Z_{N-k} is v at N-k
+      static_for<BPL>([&](auto bc) {
+        constexpr int b = decltype(bc)::value;
+        static_for<RL / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          constexpr int k = b + r * NsL;
+          if constexpr (k != 0) {
+            constexpr int mk = N - k;
+            partner[b * (RL / 2) + r] = v[(mk % NsL) * RL + mk / NsL];
+          }
+        });
+      });
+      if constexpr (DST_IN_LDS) __syncthreads();
+    } else {
+      static_for<BPL>([&](auto bc) {
+        constexpr int b = decltype(bc)::value;
+        const int g = t + b * TPR;
+        static_for<RL / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value + RL / 2;
+          lds[lds_pad(g + r * NsL - N / 2)] = v[b * RL + r];
+        });
+      });
+      __syncthreads();
+      static_for<BPL>([&](auto bc) {
+        constexpr int b = decltype(bc)::value;
+        const int g = t + b * TPR;
+        static_for<RL / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          const int k = g + r * NsL;
+          // k == 0 reads index N/2 (never written); its value is unused
+          partner[b * (RL / 2) + r] = lds[lds_pad(N / 2 - k)];
+        });
+      });
+      if constexpr (DST_IN_LDS) __syncthreads();
+    }
+    if (!active) return;
+    static_for<BPL>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int g = t + b * TPR;
+      static_for<RL / 2>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        const int k = g + r * NsL;
+        const float2 a = v[b * RL + r];
+        if (r == 0 && b == 0 && t == 0) {
+          // slot 0: (Y_0, Y_{n/2}) = (Re Z_0 + Im Z_0, Re Z_0 - Im Z_0); Y_{N/2} = conj(Z_{N/2})
+          dst.store(0, make_float2(a.x + a.y, a.x - a.y));
+          dst.store(N / 2, c_conj(v[b * RL + RL / 2]));
+        } else {
+          const float2 bc2 = c_conj(partner[b * (RL / 2) + r]);
+          const float2 s = c_add(a, bc2), d = c_sub(a, bc2);
+          const float2 w = twp[k];
+          const float2 u = make_float2(w.y, -w.x);  // -i * W_n^k
+          const float2 q = c_mul<false>(d, u);
+          dst.store(k, c_scale(c_add(s, q), 0.5f));
+          dst.store(N - k, c_conj(c_scale(c_sub(s, q), 0.5f)));
+        }
+      });
+    });
+  }
+}
+
+// ----------------------------------------------------------------------------------
+// Inverse rdFFT of one row: packed pairs P[k] (src) -> pairs (x_{2m}, x_{2m+1}) (dst).
+// SRC_IN_LDS: src lives in this row's LDS region (a barrier then separates its reads
+// from the first LDS write).
+template <int LOGN, bool SRC_IN_LDS, class Src, class Dst>
+__device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, const Dst& dst, float2* lds,
+                                            const float2* __restrict__ tw) {
+  using P = RowPlan<LOGN>;
+  constexpr int N = P::N, E = P::E, TPR = P::TPR;
+  constexpr float sc = 1.0f / (2.0f * N);  // 1/n
+  if constexpr (LOGN == 0) {
+    if (active) {
+      const float2 y = src.load(0);
+      dst.store(0, make_float2(0.5f * (y.x + y.y), 0.5f * (y.x - y.y)));
+    }
+    return;
+  } else {
+    constexpr int R0 = radix(LOGN, 0), BPT0 = E / R0;
+    const float2* __restrict__ twp = tw + post_table_offset(LOGN);
+    float2 v[E];
+    float2 mirror[E / 2];  // Z~_{N-m} for this thread's jobs m < N/2
+    static_for<BPT0>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int g = t + b * TPR;
+      static_for<R0 / 2>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        const int m = g + r * (N / R0);
+        if (!active) {
+          v[b * R0 + r] = make_float2(0.f, 0.f);
+          mirror[b * (R0 / 2) + r] = make_float2(0.f, 0.f);
+        } else if (r == 0 && b == 0 && t == 0) {
+          // Z~_0 = ((Y_0 + Y_{n/2}) + i (Y_0 - Y_{n/2})) / n ;  Z~_{N/2} = conj(Y_{N/2}) * 2/n
+          const float2 y0 = src.load(0);
+          v[b * R0 + r] = make_float2(sc * (y0.x + y0.y), sc * (y0.x - y0.y));
+          v[b * R0 + R0 / 2] = c_scale(c_conj(src.load(N / 2)), 2.0f * sc);
+          mirror[b * (R0 / 2) + r] = make_float2(0.f, 0.f);
+        } else {
+          const float2 ya = src.load(m);
+          const float2 yb = c_conj(src.load(N - m));
+          const float2 s = c_add(ya, yb), d = c_sub(ya, yb);
+          const float2 w = twp[m];
+          const float2 u = make_float2(w.y, w.x);  // i * conj(W_n^m)
+          const float2 q = c_mul<false>(d, u);
+          v[b * R0 + r] = c_scale(c_add(s, q), sc);
+          mirror[b * (R0 / 2) + r] = c_conj(c_scale(c_sub(s, q), sc));
+        }
+      });
+    });
+    if constexpr (TPR == 1) {
+      // the partner values are this thread's own upper-half inputs
+      static_for<BPT0>([&](auto bc) {
+        constexpr int b = decltype(bc)::value;
+        static_for<R0 / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          constexpr int m = b + r * (N / R0);
+          if constexpr (m != 0) {
+            constexpr int mm = N - m;
+            v[(mm % (N / R0)) * R0 + mm / (N / R0)] = mirror[b * (R0 / 2) + r];
+          }
+        });
+      });
+    } else {
+      if constexpr (SRC_IN_LDS) __syncthreads();
+      static_for<BPT0>([&](auto bc) {
+        constexpr int b = decltype(bc)::value;
+        const int g = t + b * TPR;
+        static_for<R0 / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          const int m = g + r * (N / R0);
+          if (m != 0) lds[lds_pad(N / 2 - m)] = mirror[b * (R0 / 2) + r];
+        });
+      });
+      __syncthreads();
+      static_for<BPT0>([&](auto bc) {
+        constexpr int b = decltype(bc)::value;
+        const int g = t + b * TPR;
+        static_for<R0 / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value + R0 / 2;
+          const int m = g + r * (N / R0);
+          if (m != N / 2) v[b * R0 + r] = lds[lds_pad(m - N / 2)];
+        });
+      });
+      __syncthreads();
+    }
+    stockham_from<LOGN, 0, true>(v, t, lds, tw);
+    if (!active) return;
+    constexpr int RL = radix(LOGN, P::NP - 1), BPL = E / RL, NsL = N / RL;
+    static_for<BPL>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int g = t + b * TPR;
+      static_for<RL>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        dst.store(g + r * NsL, v[b * RL + r]);
+      });
+    });
+  }
+}
+
+}  // namespace rdfft

@@ -1,0 +1,38 @@
+// launch.hpp -- host-side launchers exported by the kernel translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+#include <array>
+#include <utility>
+
+namespace rdfft {
+
+// In-place forward (inv = false) or inverse rdFFT of `rows` rows of 2^(logn+1) elements.
+hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, bool bf16, bool inv, const float2* tw,
+                             hipStream_t stream);
+
+// Copies the host twiddle table to the current device; returns its device address.
+hipError_t upload_twiddles(const void* host, size_t bytes, const float2** dev_ptr);
+
+struct BcaArgs {
+  const void* x;
+  const void* c;      // packed spectra [q][kb][p]
+  void* y;            // forward output, or backward upstream gradient gy
+  void* dx;           // backward only
+  float* dc;          // backward only
+  int64_t tokens;
+  int q, kb, logp;    // p = 2^logp
+  bool bf16;
+};
+
+hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream);
+// also zeroes dc first and transforms it to the time domain afterwards
+hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu);
+
+// whether the fused kernels handle p = 2^logp with q x kb blocks
+bool bca_shape_supported(int logp, int q, int kb);
+
+}  // namespace rdfft

@@ -1,0 +1,104 @@
+// plan.hpp -- compile-time transform plans and twiddle-table layout.
+//
+// A real row of n = 2N samples is viewed as N complex points z_m = x_{2m} + i x_{2m+1}
+// (the interleaved pairs already are that view).  The row transform computes the
+// N-point complex DFT of z with a Stockham (self-sorting) sequence of radix passes
+// held in registers and exchanged through LDS, then the real-to-packed post-pass
+// that turns Z into the n/2+1 real-signal bins Y_k (Sec. 4.1, "Squeeze N+2 into N").
+//
+// Shared by the host table generator and the device kernels of this library.
+#pragma once
+
+#include <stdint.h>
+
+namespace rdfft {
+
+constexpr int kMaxLogN = 15;  // N = 32768 complex points, n = 65536 reals
+
+// Radix sequence per log2(N).  Pass q multiplies the sub-transform size by kPlan[q].
+constexpr int kPlan[kMaxLogN + 1][5] = {
+    {0},              // N = 1: handled by the post-pass alone
+    {2},              // 2
+    {4},              // 4
+    {8},              // 8
+    {16},             // 16
+    {8, 4},           // 32
+    {8, 8},           // 64
+    {16, 8},          // 128
+    {16, 16},         // 256
+    {8, 8, 8},        // 512
+    {16, 8, 8},       // 1024
+    {16, 16, 8},      // 2048
+    {16, 16, 16},     // 4096
+    {16, 16, 8, 4},   // 8192
+    {16, 16, 16, 4},  // 16384
+    {16, 16, 16, 8},  // 32768
+};
+
+// Complex values each thread holds (E) and LDS exchange chunks (C).  With C > 1 a
+// pass-to-pass exchange is split into C rounds so that one round fits in LDS.
+constexpr int kElems[kMaxLogN + 1] = {1, 2, 4, 8, 16, 8, 8, 16, 16, 8, 16, 16, 16, 16, 16, 32};
+constexpr int kChunks[kMaxLogN + 1] = {1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 2};
+
+constexpr int num_passes(int logn) {
+  int k = 0;
+  while (k < 5 && kPlan[logn][k] != 0) ++k;
+  return k;
+}
+
+constexpr int radix(int logn, int q) { return kPlan[logn][q]; }
+
+// product of the radices of passes before q
+constexpr int stride_before(int logn, int q) {
+  int s = 1;
+  for (int i = 0; i < q; ++i) s *= kPlan[logn][i];
+  return s;
+}
+
+constexpr bool plan_is_consistent(int logn) {
+  int prod = 1;
+  for (int q = 0; q < num_passes(logn); ++q) {
+    prod *= radix(logn, q);
+    if (kElems[logn] % radix(logn, q) != 0) return false;
+  }
+  return prod == (1 << logn);
+}
+
+// Twiddles of pass q >= 1: W_{Ns*R}^{r*k}, k < Ns, 1 <= r < R, stored at [(r-1)*Ns + k].
+constexpr int pass_table_size(int logn, int q) {
+  return q == 0 ? 0 : (radix(logn, q) - 1) * stride_before(logn, q);
+}
+
+// Post-pass twiddles W_n^k = exp(-2 pi i k / (2N)), 0 <= k < N/2.
+constexpr int post_table_size(int logn) { return (1 << logn) / 2; }
+
+constexpr int plan_table_size(int logn) {
+  int s = 0;
+  for (int q = 0; q < num_passes(logn); ++q) s += pass_table_size(logn, q);
+  return s + post_table_size(logn);
+}
+
+constexpr int plan_table_offset(int logn) {
+  int s = 0;
+  for (int l = 0; l < logn; ++l) s += plan_table_size(l);
+  return s;
+}
+
+constexpr int pass_table_offset(int logn, int q) {
+  int s = plan_table_offset(logn);
+  for (int i = 0; i < q; ++i) s += pass_table_size(logn, i);
+  return s;
+}
+
+constexpr int post_table_offset(int logn) {
+  return plan_table_offset(logn) + plan_table_size(logn) - post_table_size(logn);
+}
+
+constexpr int kTableEntries = plan_table_offset(kMaxLogN + 1);  // float2 entries
+
+// LDS padding: one float2 of padding after every 16, so that the strided
+// Stockham writes of the early passes spread over all banks.
+constexpr int lds_pad(int i) { return i + (i >> 4); }
+constexpr int lds_padded_size(int count) { return count + (count >> 4) + 1; }
+
+}  // namespace rdfft

@@ -1,0 +1,78 @@
+// rdfft_kernels.hip -- batched in-place rdFFT / irdFFT row kernels and the twiddle table.
+//
+// A workgroup owns RW whole rows (RowPlan::RW); every row is read once from HBM into
+// registers, transformed through LDS, and written back to the same addresses, so the
+// call needs no memory beyond the caller's buffer (Sec. 4.1, rdFFT algorithm).
+#include <hip/hip_runtime.h>
+
+#include "fft_device.hpp"
+#include "launch.hpp"
+
+namespace rdfft {
+
+// The library's only device-resident data: the twiddle factors of every plan.
+__device__ float2 g_twiddles[kTableEntries];
+
+template <int LOGN, class Acc, class Elem, bool INV>
+__global__ void __launch_bounds__(RowPlan<LOGN>::WG) rdfft_rows_kernel(Elem* buf, int64_t rows,
+                                                                        const float2* __restrict__ tw) {
+  using P = RowPlan<LOGN>;
+  constexpr int LDS_ROW = P::LDS_F2 > 0 ? P::LDS_F2 : 1;
+  __shared__ float2 lds[P::RW * LDS_ROW];
+  const int tid = threadIdx.x;
+  const int rho = tid / P::TPR;
+  const int t = tid - rho * P::TPR;
+  const int64_t row = (int64_t)blockIdx.x * P::RW + rho;
+  const bool active = row < rows;
+  const Acc acc{buf + (active ? row : 0) * (int64_t)P::N};
+  float2* my = lds + rho * LDS_ROW;
+  if constexpr (!INV) row_forward<LOGN, false>(t, active, acc, acc, my, tw);
+  else row_inverse<LOGN, false>(t, active, acc, acc, my, tw);
+}
+
+template <int LOGN, class Acc, class Elem, bool INV>
+static hipError_t launch_rows(void* buf, int64_t rows, const float2* tw, hipStream_t stream) {
+  using P = RowPlan<LOGN>;
+  // keep every launch within the grid limit
+  const int64_t max_blocks = (int64_t)1 << 30;
+  Elem* base = static_cast<Elem*>(buf);
+  for (int64_t r0 = 0; r0 < rows;) {
+    const int64_t blocks = std::min<int64_t>((rows - r0 + P::RW - 1) / P::RW, max_blocks);
+    const int64_t nrows = std::min<int64_t>(blocks * P::RW, rows - r0);
+    hipLaunchKernelGGL((rdfft_rows_kernel<LOGN, Acc, Elem, INV>), dim3((unsigned)blocks), dim3(P::WG), 0, stream,
+                       base + r0 * (int64_t)P::N, nrows, tw);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    r0 += nrows;
+  }
+  return hipSuccess;
+}
+
+using RowLauncher = hipError_t (*)(void*, int64_t, const float2*, hipStream_t);
+
+template <int... L>
+static std::array<RowLauncher, sizeof...(L)> make_row_table(bool bf16, bool inv, std::integer_sequence<int, L...>) {
+  return {(bf16 ? (inv ? &launch_rows<L, GlobalBF16, uint32_t, true> : &launch_rows<L, GlobalBF16, uint32_t, false>)
+                : (inv ? &launch_rows<L, GlobalF32, float2, true> : &launch_rows<L, GlobalF32, float2, false>))...};
+}
+
+hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, bool bf16, bool inv, const float2* tw,
+                             hipStream_t stream) {
+  static const auto seq = std::make_integer_sequence<int, kMaxLogN + 1>{};
+  static const std::array<RowLauncher, kMaxLogN + 1> tables[4] = {
+      make_row_table(false, false, seq), make_row_table(false, true, seq), make_row_table(true, false, seq),
+      make_row_table(true, true, seq)};
+  return tables[(bf16 ? 2 : 0) + (inv ? 1 : 0)][logn](buf, rows, tw, stream);
+}
+
+hipError_t upload_twiddles(const void* host, size_t bytes, const float2** dev_ptr) {
+  hipError_t e = hipMemcpyToSymbol(HIP_SYMBOL(g_twiddles), host, bytes, 0, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return e;
+  void* p = nullptr;
+  e = hipGetSymbolAddress(&p, HIP_SYMBOL(g_twiddles));
+  if (e != hipSuccess) return e;
+  *dev_ptr = static_cast<const float2*>(p);
+  return hipSuccess;
+}
+
+}  // namespace rdfft

@@ -1,0 +1,69 @@
+"""Helpers shared by the GPU parity tests: host<->device copies of seeded inputs and
+the comparison rule.
+
+Comparison rule (both must hold):
+* relative L2 error over the compared outputs, ||gpu - ref||_2 / ||ref||_2, at most
+  1e-5 for float32 storage and 2e-2 for bfloat16 storage, the reference being the
+  float64 oracle on the same stored inputs;
+* element by element, |gpu - ref| <= 2^-8 |ref| (bf16 only: one round-to-nearest-even
+  store) + 2e-5 * rms(ref of that row) (float32 arithmetic).
+"""
+
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from paper_2511_01385_amd import inputs
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+
+
+def to_device(stored: np.ndarray, dtype: str, device="cuda") -> torch.Tensor:
+    if dtype == "f32":
+        return torch.from_numpy(np.ascontiguousarray(stored, dtype=np.float32)).to(device)
+    bits = np.ascontiguousarray(stored, dtype=np.uint16).view(np.int16)
+    return torch.from_numpy(bits).view(torch.bfloat16).to(device)
+
+
+def to_host_f64(t: torch.Tensor) -> np.ndarray:
+    t = t.detach().cpu()
+    if t.dtype == torch.float32:
+        return t.numpy().astype(np.float64)
+    if t.dtype == torch.bfloat16:
+        return inputs.to_f64(t.view(torch.int16).numpy().view(np.uint16), "bf16")
+    raise TypeError(t.dtype)
+
+
+def rel_l2(got: np.ndarray, ref: np.ndarray) -> float:
+    den = np.linalg.norm(ref)
+    return float(np.linalg.norm(got - ref) / (den if den > 0 else 1.0))
+
+
+def assert_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "") -> float:
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    assert np.all(np.isfinite(got)), f"{what}: non-finite output"
+    err = rel_l2(got, ref)
+    assert err <= TOL[dtype], f"{what}: rel-L2 {err:.3e} > {TOL[dtype]:.1e}"
+    r2 = ref.reshape(-1, ref.shape[-1]) if ref.ndim > 1 else ref.reshape(1, -1)
+    g2 = got.reshape(r2.shape)
+    rms = np.sqrt(np.mean(r2**2, axis=1, keepdims=True))
+    bound = 2e-5 * rms + (2.0**-8 * np.abs(r2) if dtype == "bf16" else 0.0)
+    bad = np.abs(g2 - r2) > bound
+    if bad.any():
+        i, j = np.argwhere(bad)[0]
+        raise AssertionError(
+            f"{what}: {int(bad.sum())} elements outside the element bound; first at row {i} col {j}: "
+            f"gpu {g2[i, j]!r} ref {r2[i, j]!r} bound {bound[i, j] if np.ndim(bound) else bound!r}"
+        )
+    return err
+
+
+def sample_rows(rows: int, count: int, seed: int) -> np.ndarray:
+    """A sorted sample of row indices that always includes the first and the last row."""
+    rng = np.random.default_rng(seed)
+    pick = rng.choice(rows, size=min(count, rows), replace=False)
+    return np.unique(np.concatenate([pick, [0, rows - 1]]))

@@ -1,0 +1,155 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point that
+include/rdfft.h declares, imports no device allocator, and rejects invalid arguments
+on the host before any HIP call (every case below must fail validation, so nothing
+is ever launched from here)."""
+
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2511_01385_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "rdfft.h")
+
+EINVAL, EUNSUP, OK = _lib.RDFFT_EINVAL, _lib.RDFFT_EUNSUPPORTED, _lib.RDFFT_OK
+F32, BF16 = _lib.RDFFT_F32, _lib.RDFFT_BF16
+
+# fake, never dereferenced addresses (validation rejects every call that uses them)
+A = 0x7F0000000000
+B = A + (1 << 30)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2511_01385_amd.build import build
+
+        build(verbose=False)
+    return _lib.load()
+
+
+def _declared():
+    text = open(HEADER).read()
+    return re.findall(r"RDFFT_API\s+[\w\s\*]+?\b(\w+)\s*\(", text)
+
+
+def test_header_declares_the_binding_names():
+    assert sorted(_declared()) == sorted(_lib.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    for name in _declared():
+        assert name in exported, name
+        assert hasattr(lib, name)
+    # nothing else leaks out of the C ABI
+    assert {n for n in exported if not n.startswith("_")} == set(_declared())
+
+
+def test_library_imports_no_device_allocator(lib):
+    out = subprocess.run(["nm", "-D", "--undefined-only", _lib.LIB_PATH], capture_output=True, text=True, check=True).stdout
+    names = {line.split()[-1].split("@")[0] for line in out.splitlines() if line.strip()}
+    bad = {n for n in names if re.match(r"hip(Malloc|MallocAsync|MallocManaged|HostMalloc|ExtMallocWithFlags|MallocPitch|Free|FreeAsync|HostRegister)", n)}
+    assert not bad, bad
+
+
+def test_status_strings(lib):
+    for code in (OK, EINVAL, EUNSUP, _lib.RDFFT_ELAUNCH, _lib.RDFFT_EDEVICE):
+        assert _lib.status_string(code).startswith("RDFFT_")
+    assert 0 < lib.rdfft_table_bytes() < (1 << 21)
+
+
+@pytest.mark.parametrize(
+    "args,want",
+    [
+        ((0, 4, 64, F32), EINVAL),  # null buffer
+        ((A + 8, 4, 64, F32), EINVAL),  # misaligned
+        ((A, -1, 64, F32), EINVAL),  # negative rows
+        ((A, 4, 63, F32), EINVAL),  # odd length: no Nyquist bin
+        ((A, 4, 1, F32), EINVAL),
+        ((A, 4, 0, F32), EINVAL),
+        ((A, 4, -8, F32), EINVAL),
+        ((A, 4, 64, 2), EINVAL),  # unknown dtype
+        ((A, 4, 96, F32), EUNSUP),  # even, not a power of two
+        ((A, 4, 131072, BF16), EUNSUP),  # beyond 65536
+        ((A, 1 << 62, 65536, F32), EINVAL),  # size overflow
+    ],
+)
+def test_transform_validation(lib, args, want):
+    for fn in (lib.rdfft_forward, lib.rdfft_inverse):
+        assert fn(args[0], args[1], args[2], args[3], None) == want
+
+
+def test_zero_rows_is_a_no_op(lib):
+    # returns before any HIP call, so a null buffer is fine
+    assert lib.rdfft_forward(None, 0, 64, F32, None) == OK
+    assert lib.rdfft_inverse(None, 0, 4096, BF16, None) == OK
+
+
+def _grads(dx, dc):
+    return ctypes.byref(_lib.BcaGrads(dx, dc))
+
+
+@pytest.mark.parametrize(
+    "x,c,y,d_in,d_out,p,tokens,dtype,want",
+    [
+        (A, B, A + (1 << 29), 256, 256, 96, 8, F32, EINVAL),  # p does not divide d
+        (A, B, A + (1 << 29), 256, 192, 128, 8, F32, EINVAL),  # p does not divide d_out
+        (A, B, A + (1 << 29), 96, 96, 48, 8, F32, EUNSUP),  # even, not a power of two
+        (A, B, A + (1 << 29), 32768, 32768, 16384, 8, F32, EUNSUP),  # p beyond 8192
+        (A, B, A + (1 << 29), 256, 256, 7, 8, F32, EINVAL),  # odd p
+        (A, B, A + (1 << 29), 256, 256, 64, -1, F32, EINVAL),
+        (A, B, A + (1 << 29), 0, 256, 64, 8, F32, EINVAL),
+        (A, B, A + (1 << 29), 256, 256, 64, 8, 5, EINVAL),
+        (0, B, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # null x
+        (A, 0, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # null spectra
+        (A, B, 0, 256, 256, 64, 8, F32, EINVAL),  # null y
+        (A + 4, B, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # misaligned
+        (A, B, A + 64, 256, 256, 64, 8, F32, EINVAL),  # y overlaps x without being x
+        (A, B, A, 256, 512, 64, 8, F32, EINVAL),  # y == x needs d_in == d_out
+        (A, A + 256, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # spectra overlap x
+    ],
+)
+def test_bca_forward_validation(lib, x, c, y, d_in, d_out, p, tokens, dtype, want):
+    assert lib.bca_forward(x, c, y, None, d_in, d_out, p, tokens, dtype, None) == want
+
+
+def test_bca_forward_rejects_grads(lib):
+    assert lib.bca_forward(A, B, A + (1 << 29), _grads(A, B), 256, 256, 64, 8, F32, None) == EINVAL
+
+
+def test_bca_forward_zero_tokens(lib):
+    assert lib.bca_forward(None, B, None, None, 256, 256, 64, 0, F32, None) == OK
+
+
+G = A + (1 << 29)  # gy
+DX = A + (2 << 29)
+DC = A + (3 << 29)
+
+
+@pytest.mark.parametrize(
+    "x,gy,dx,dc,d_in,d_out,want",
+    [
+        (A, G, DX, 0, 256, 256, EINVAL),  # null dc
+        (A, G, 0, DC, 256, 256, EINVAL),  # null dx
+        (A, G, DX, DC + 4, 256, 256, EINVAL),  # misaligned dc
+        (A, A + 512, DX, DC, 256, 256, EINVAL),  # gy overlaps x
+        (A, G, A, DC, 256, 256, EINVAL),  # dx overlaps x
+        (A, G, G, DC, 256, 512, EINVAL),  # dx == gy needs d_in == d_out
+        (A, G, G + 64, DC, 256, 256, EINVAL),  # dx overlaps gy without being gy
+        (A, G, DX, A + 128, 256, 256, EINVAL),  # dc overlaps x
+        (A, G, DX, DX, 256, 256, EINVAL),  # dc overlaps dx
+        (A, G, DX, B, 256, 256, EINVAL),  # dc overlaps the spectra
+    ],
+)
+def test_bca_backward_validation(lib, x, gy, dx, dc, d_in, d_out, want):
+    assert lib.bca_backward(x, B, gy, _grads(dx, dc), d_in, d_out, 64, 8, F32, None) == want
+
+
+def test_bca_backward_needs_grads(lib):
+    assert lib.bca_backward(A, B, G, None, 256, 256, 64, 8, F32, None) == EINVAL
