@@ -301,14 +301,10 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
   using P = RowPlan<LOGN>;
   constexpr int N = P::N, E = P::E, TPR = P::TPR;
   if constexpr (LOGN == 0) {
-    // n = 2: Y_0 = x0 + x1, Y_1 = x0 - x1
-    if (active) {
-      const float2 z = src.load(0);
-      if constexpr (DST_IN_LDS) __syncthreads();
-      dst.store(0, make_float2(z.x + z.y, z.x - z.y));
-    } else if constexpr (DST_IN_LDS) {
-      __syncthreads();
-    }
+    // n = 2: Y_0 = x0 + x1, Y_1 = x0 - x1.  The barrier stays outside any branch.
+    const float2 z = src.load(0);
+    if constexpr (DST_IN_LDS) __syncthreads();
+    if (active) dst.store(0, make_float2(z.x + z.y, z.x - z.y));
     return;
   } else {
     float2 v[E];
@@ -318,7 +314,9 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
       const int g = t + b * TPR;
       static_for<R0>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
-        v[b * R0 + r] = active ? src.load(g + r * (N / R0)) : make_float2(0.f, 0.f);
+        // unconditional: inactive rows point at a valid row, so the loads stay in
+        // bounds and all of them are in flight at once
+        v[b * R0 + r] = src.load(g + r * (N / R0));
       });
     });
     stockham_from<LOGN, 0, false>(v, t, lds, tw);
@@ -337,6 +335,8 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
           if constexpr (k != 0) {
             constexpr int mk = N - k;
             partner[b * (RL / 2) + r] = v[(mk % NsL) * RL + mk / NsL];
+          } else {
+            partner[b * (RL / 2) + r] = make_float2(0.f, 0.f);  // unused: slot 0 is special
           }
         });
       });
@@ -371,19 +371,25 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
         constexpr int r = decltype(rc)::value;
         const int k = g + r * NsL;
         const float2 a = v[b * RL + r];
-        if (r == 0 && b == 0 && t == 0) {
-          // slot 0: (Y_0, Y_{n/2}) = (Re Z_0 + Im Z_0, Re Z_0 - Im Z_0); Y_{N/2} = conj(Z_{N/2})
-          dst.store(0, make_float2(a.x + a.y, a.x - a.y));
-          dst.store(N / 2, c_conj(v[b * RL + RL / 2]));
-        } else {
-          const float2 bc2 = c_conj(partner[b * (RL / 2) + r]);
-          const float2 s = c_add(a, bc2), d = c_sub(a, bc2);
-          const float2 w = twp[k];
-          const float2 u = make_float2(w.y, -w.x);  // -i * W_n^k
-          const float2 q = c_mul<false>(d, u);
-          dst.store(k, c_scale(c_add(s, q), 0.5f));
-          dst.store(N - k, c_conj(c_scale(c_sub(s, q), 0.5f)));
+        const float2 bc2 = c_conj(partner[b * (RL / 2) + r]);
+        const float2 s = c_add(a, bc2), d = c_sub(a, bc2);
+        const float2 w = twp[k];                    // W_n^k (k = 0 reads W^0 = 1)
+        const float2 u = make_float2(w.y, -w.x);  // -i * W_n^k
+        const float2 q = c_mul<false>(d, u);
+        float2 lo = c_scale(c_add(s, q), 0.5f);
+        float2 hi = c_conj(c_scale(c_sub(s, q), 0.5f));
+        int hi_idx = N - k;
+        if constexpr (b == 0 && r == 0) {
+          // k == 0 (thread 0): slot 0 = (Y_0, Y_{n/2}) = (Re Z_0 + Im Z_0, Re Z_0 - Im Z_0)
+          // and Y_{N/2} = conj(Z_{N/2}); chosen by selects so the stores stay uniform
+          const bool z = t == 0;
+          const float2 zh = c_conj(v[RL / 2]);
+          lo = z ? make_float2(a.x + a.y, a.x - a.y) : lo;
+          hi = z ? zh : hi;
+          hi_idx = z ? N / 2 : hi_idx;
         }
+        dst.store(k, lo);
+        dst.store(hi_idx, hi);
       });
     });
   }
@@ -400,10 +406,8 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
   constexpr int N = P::N, E = P::E, TPR = P::TPR;
   constexpr float sc = 1.0f / (2.0f * N);  // 1/n
   if constexpr (LOGN == 0) {
-    if (active) {
-      const float2 y = src.load(0);
-      dst.store(0, make_float2(0.5f * (y.x + y.y), 0.5f * (y.x - y.y)));
-    }
+    const float2 y = src.load(0);
+    if (active) dst.store(0, make_float2(0.5f * (y.x + y.y), 0.5f * (y.x - y.y)));
     return;
   } else {
     constexpr int R0 = radix(LOGN, 0), BPT0 = E / R0;
@@ -416,25 +420,24 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
       static_for<R0 / 2>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
         const int m = g + r * (N / R0);
-        if (!active) {
-          v[b * R0 + r] = make_float2(0.f, 0.f);
-          mirror[b * (R0 / 2) + r] = make_float2(0.f, 0.f);
-        } else if (r == 0 && b == 0 && t == 0) {
+        // m == 0 only for thread 0 at (b, r) = (0, 0); it pairs with slot N/2 instead of N
+        const bool z = (b == 0 && r == 0) ? (t == 0) : false;
+        const float2 ya = src.load(m);
+        const float2 yraw = src.load(z ? N / 2 : N - m);
+        const float2 yb = c_conj(yraw);
+        const float2 s = c_add(ya, yb), d = c_sub(ya, yb);
+        const float2 w = twp[m];
+        const float2 u = make_float2(w.y, w.x);  // i * conj(W_n^m)
+        const float2 q = c_mul<false>(d, u);
+        float2 lo = c_scale(c_add(s, q), sc);
+        float2 hi = c_conj(c_scale(c_sub(s, q), sc));
+        if constexpr (b == 0 && r == 0) {
           // Z~_0 = ((Y_0 + Y_{n/2}) + i (Y_0 - Y_{n/2})) / n ;  Z~_{N/2} = conj(Y_{N/2}) * 2/n
-          const float2 y0 = src.load(0);
-          v[b * R0 + r] = make_float2(sc * (y0.x + y0.y), sc * (y0.x - y0.y));
-          v[b * R0 + R0 / 2] = c_scale(c_conj(src.load(N / 2)), 2.0f * sc);
-          mirror[b * (R0 / 2) + r] = make_float2(0.f, 0.f);
-        } else {
-          const float2 ya = src.load(m);
-          const float2 yb = c_conj(src.load(N - m));
-          const float2 s = c_add(ya, yb), d = c_sub(ya, yb);
-          const float2 w = twp[m];
-          const float2 u = make_float2(w.y, w.x);  // i * conj(W_n^m)
-          const float2 q = c_mul<false>(d, u);
-          v[b * R0 + r] = c_scale(c_add(s, q), sc);
-          mirror[b * (R0 / 2) + r] = c_conj(c_scale(c_sub(s, q), sc));
+          lo = z ? make_float2(sc * (ya.x + ya.y), sc * (ya.x - ya.y)) : lo;
+          v[R0 / 2] = c_scale(yb, 2.0f * sc);  // only kept by thread 0 (others overwrite it below)
         }
+        v[b * R0 + r] = lo;
+        mirror[b * (R0 / 2) + r] = hi;
       });
     });
     if constexpr (TPR == 1) {
