@@ -199,6 +199,12 @@ struct LdsSpectrum {
   __device__ __forceinline__ void store(int m, float2 v) const { base[lds_pad(m)] = v; }
 };
 
+// lds_pad(base + j*stride) == lds_pad(base) + pad_step(j*stride) whenever the low four
+// bits of base plus those of j*stride stay below 16.  Every Stockham exchange address has
+// that form (base's low bits are below the sub-transform stride, or the stride is a
+// multiple of 16), so one padded base per butterfly plus compile-time offsets suffices.
+constexpr int pad_step(int d) { return d + (d >> 4); }
+
 // ----------------------------------------------------------------------------------
 template <int LOGN>
 struct RowPlan {
@@ -223,7 +229,8 @@ __device__ __forceinline__ void stockham_compute(float2* v, int t, const float2*
   constexpr int Ns = stride_before(LOGN, Q);
   constexpr int BPT = P::E / R;
   if constexpr (Q > 0) {
-    const float2* __restrict__ twq = tw + pass_table_offset(LOGN, Q);
+    constexpr int kOff = pass_table_offset(LOGN, Q);  // forced to a compile-time constant
+    const float2* __restrict__ twq = tw + kOff;
     static_for<BPT>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * P::TPR;
@@ -257,20 +264,21 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
       if constexpr (b / (BPT / C) == c) {
         const int g = t + b * TPR;
         const int k = g & (Ns - 1);
-        const int base = (g - k) * R + k - c * CH;
+        const int pb = lds_pad((g - k) * R + k - c * CH);
         static_for<R>([&](auto rc) {
           constexpr int r = decltype(rc)::value;
-          lds[lds_pad(base + r * Ns)] = v[b * R + r];
+          lds[pb + pad_step(r * Ns)] = v[b * R + r];
         });
       }
     });
     __syncthreads();
     static_for<BPT2>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
-      const int g = t + b * TPR;
+      const int pg = lds_pad(t + b * TPR);
       static_for<R2>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
-        if constexpr (r / (R2 / C) == c) nv[b * R2 + r] = lds[lds_pad(g + r * (N / R2) - c * CH)];
+        // chunk c starts at r = c*R2/C, i.e. at index c*CH: the address is g + (r - c*R2/C)*(N/R2)
+        if constexpr (r / (R2 / C) == c) nv[b * R2 + r] = lds[pg + pad_step((r - c * (R2 / C)) * (N / R2))];
       });
     });
     __syncthreads();
@@ -323,7 +331,8 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
 
     // Post-pass.  After the last pass thread t holds Z_m at m = g_b + r*(N/RL).
     constexpr int RL = radix(LOGN, P::NP - 1), BPL = E / RL, NsL = N / RL;
-    const float2* __restrict__ twp = tw + post_table_offset(LOGN);
+    constexpr int kPostOff = post_table_offset(LOGN);
+    const float2* __restrict__ twp = tw + kPostOff;
     float2 partner[E / 2];
     if constexpr (TPR == 1) {
       // the whole row is in this thread's registers: Z_{N-k} is v at N-k
@@ -344,21 +353,26 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
     } else {
       static_for<BPL>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
-        const int g = t + b * TPR;
+        const int pg = lds_pad(t + b * TPR);
         static_for<RL / 2>([&](auto rc) {
-          constexpr int r = decltype(rc)::value + RL / 2;
-          lds[lds_pad(g + r * NsL - N / 2)] = v[b * RL + r];
+          constexpr int r = decltype(rc)::value;  // element r + RL/2 sits at g + r*NsL past N/2
+          lds[pg + pad_step(r * NsL)] = v[b * RL + r + RL / 2];
         });
       });
       __syncthreads();
       static_for<BPL>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
         const int g = t + b * TPR;
+        // Z_{N-k} for k = g + r*NsL sits at N/2 - k = (NsL - g) + (RL/2 - 1 - r)*NsL;
+        // k == 0 reads index N/2 (never written); its value is unused
+        const int pq = lds_pad(NsL - g);
         static_for<RL / 2>([&](auto rc) {
           constexpr int r = decltype(rc)::value;
-          const int k = g + r * NsL;
-          // k == 0 reads index N/2 (never written); its value is unused
-          partner[b * (RL / 2) + r] = lds[lds_pad(N / 2 - k)];
+          if constexpr (NsL % 16 == 0) {
+            partner[b * (RL / 2) + r] = lds[pq + pad_step((RL / 2 - 1 - r) * NsL)];
+          } else {
+            partner[b * (RL / 2) + r] = lds[lds_pad(N / 2 - g - r * NsL)];
+          }
         });
       });
       if constexpr (DST_IN_LDS) __syncthreads();
@@ -373,11 +387,11 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
         const float2 a = v[b * RL + r];
         const float2 bc2 = c_conj(partner[b * (RL / 2) + r]);
         const float2 s = c_add(a, bc2), d = c_sub(a, bc2);
-        const float2 w = twp[k];                    // W_n^k (k = 0 reads W^0 = 1)
-        const float2 u = make_float2(w.y, -w.x);  // -i * W_n^k
-        const float2 q = c_mul<false>(d, u);
-        float2 lo = c_scale(c_add(s, q), 0.5f);
-        float2 hi = c_conj(c_scale(c_sub(s, q), 0.5f));
+        // Y_k = s/2 + (-i W_n^k / 2) d,  Y_{N-k} = conj(s/2 - (-i W_n^k / 2) d); the table holds
+        // -i W_n^k / 2 (k = 0 reads an entry whose result the slot-0 select replaces)
+        const float2 q = c_mul<false>(d, twp[k]);
+        float2 lo = make_float2(fmaf(s.x, 0.5f, q.x), fmaf(s.y, 0.5f, q.y));
+        float2 hi = make_float2(fmaf(s.x, 0.5f, -q.x), -fmaf(s.y, 0.5f, -q.y));
         int hi_idx = N - k;
         if constexpr (b == 0 && r == 0) {
           // k == 0 (thread 0): slot 0 = (Y_0, Y_{n/2}) = (Re Z_0 + Im Z_0, Re Z_0 - Im Z_0)
@@ -411,9 +425,11 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
     return;
   } else {
     constexpr int R0 = radix(LOGN, 0), BPT0 = E / R0;
-    const float2* __restrict__ twp = tw + post_table_offset(LOGN);
+    constexpr int kPostOff = post_table_offset(LOGN);
+    const float2* __restrict__ twp = tw + kPostOff;
     float2 v[E];
     float2 mirror[E / 2];  // Z~_{N-m} for this thread's jobs m < N/2
+    float2 zhalf;          // Z~_{N/2} = conj(Y_{N/2}) * 2/n (meaningful in thread 0 only)
     static_for<BPT0>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * TPR;
@@ -426,15 +442,15 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
         const float2 yraw = src.load(z ? N / 2 : N - m);
         const float2 yb = c_conj(yraw);
         const float2 s = c_add(ya, yb), d = c_sub(ya, yb);
-        const float2 w = twp[m];
-        const float2 u = make_float2(w.y, w.x);  // i * conj(W_n^m)
-        const float2 q = c_mul<false>(d, u);
-        float2 lo = c_scale(c_add(s, q), sc);
-        float2 hi = c_conj(c_scale(c_sub(s, q), sc));
+        // Z~_m = (s + i conj(W_n^m) d) / n,  Z~_{N-m} = conj(s - i conj(W_n^m) d) / n; the table
+        // holds i conj(W_n^m) / n
+        const float2 q = c_mul<false>(d, twp[N / 2 + m]);
+        float2 lo = make_float2(fmaf(s.x, sc, q.x), fmaf(s.y, sc, q.y));
+        float2 hi = make_float2(fmaf(s.x, sc, -q.x), -fmaf(s.y, sc, -q.y));
         if constexpr (b == 0 && r == 0) {
           // Z~_0 = ((Y_0 + Y_{n/2}) + i (Y_0 - Y_{n/2})) / n ;  Z~_{N/2} = conj(Y_{N/2}) * 2/n
           lo = z ? make_float2(sc * (ya.x + ya.y), sc * (ya.x - ya.y)) : lo;
-          v[R0 / 2] = c_scale(yb, 2.0f * sc);  // only kept by thread 0 (others overwrite it below)
+          zhalf = c_scale(yb, 2.0f * sc);
         }
         v[b * R0 + r] = lo;
         mirror[b * (R0 / 2) + r] = hi;
@@ -442,6 +458,7 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
     });
     if constexpr (TPR == 1) {
       // the partner values are this thread's own upper-half inputs
+      v[R0 / 2] = zhalf;
       static_for<BPT0>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
         static_for<R0 / 2>([&](auto rc) {
@@ -455,23 +472,32 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
       });
     } else {
       if constexpr (SRC_IN_LDS) __syncthreads();
+      constexpr int S0 = N / R0;
       static_for<BPT0>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
         const int g = t + b * TPR;
+        // Z~_{N-m} for m = g + r*S0 goes to N/2 - m = (S0 - g) + (R0/2 - 1 - r)*S0; the
+        // m == 0 element (thread 0) lands on index N/2, which nobody reads
+        const int pq = lds_pad(S0 - g);
         static_for<R0 / 2>([&](auto rc) {
           constexpr int r = decltype(rc)::value;
-          const int m = g + r * (N / R0);
-          if (m != 0) lds[lds_pad(N / 2 - m)] = mirror[b * (R0 / 2) + r];
+          if constexpr (S0 % 16 == 0) {
+            lds[pq + pad_step((R0 / 2 - 1 - r) * S0)] = mirror[b * (R0 / 2) + r];
+          } else {
+            lds[lds_pad(N / 2 - g - r * S0)] = mirror[b * (R0 / 2) + r];
+          }
         });
       });
+      // element m = N/2 (thread 0) reads index 0, which no mirror write touches
+      if (t == 0) lds[0] = zhalf;
       __syncthreads();
       static_for<BPT0>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
         const int g = t + b * TPR;
+        const int pg = lds_pad(g);
         static_for<R0 / 2>([&](auto rc) {
-          constexpr int r = decltype(rc)::value + R0 / 2;
-          const int m = g + r * (N / R0);
-          if (m != N / 2) v[b * R0 + r] = lds[lds_pad(m - N / 2)];
+          constexpr int r = decltype(rc)::value;  // element r + R0/2 is at m - N/2 = g + r*S0
+          v[b * R0 + r + R0 / 2] = lds[pg + pad_step(r * S0)];
         });
       });
       __syncthreads();

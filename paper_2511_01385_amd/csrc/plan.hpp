@@ -69,8 +69,10 @@ constexpr int pass_table_size(int logn, int q) {
   return q == 0 ? 0 : (radix(logn, q) - 1) * stride_before(logn, q);
 }
 
-// Post-pass twiddles W_n^k = exp(-2 pi i k / (2N)), 0 <= k < N/2.
-constexpr int post_table_size(int logn) { return (1 << logn) / 2; }
+// Post-pass twiddles, 0 <= k < N/2, with the post-pass scale folded in (exact: powers of two):
+//   forward  [k]       = (1/2) * (-i) * W_n^k
+//   inverse  [N/2 + k] = (1/n) * i * conj(W_n^k),   W_n^k = exp(-2 pi i k / (2N)).
+constexpr int post_table_size(int logn) { return 2 * ((1 << logn) / 2); }
 
 constexpr int plan_table_size(int logn) {
   int s = 0;

@@ -44,7 +44,12 @@ std::vector<HostC32> build_twiddle_table() {
         for (int k = 0; k < Ns; ++k) t[(size_t)off + (size_t)(r - 1) * Ns + k] = unit_root((long long)r * k, (long long)Ns * R);
     }
     const int N = 1 << logn, off = post_table_offset(logn);
-    for (int k = 0; k < N / 2; ++k) t[(size_t)off + k] = unit_root(k, 2LL * N);
+    const float inv_n = 1.0f / (2.0f * (float)N);
+    for (int k = 0; k < N / 2; ++k) {
+      const HostC32 w = unit_root(k, 2LL * N);                      // (cos, -sin)
+      t[(size_t)off + k] = HostC32{0.5f * w.y, -0.5f * w.x};         // (1/2) (-i) W
+      t[(size_t)off + N / 2 + k] = HostC32{inv_n * w.y, inv_n * w.x};  // (1/n) i conj(W)
+    }
   }
   return t;
 }
