@@ -4,13 +4,15 @@
 // tile in LDS, in the packed pair layout of the row transforms:
 //   forward : X_j = rdFFT(x_j)  ->  Y_i = sum_j C_ij . X_j  ->  y_i = irdFFT(Y_i)
 //   backward: X_j = rdFFT(x_j), G_i = rdFFT(g_i)
-//             dC_ij += conj(X_j) . G_i          (float32 accumulators in registers)
+//             dC_ij += conj(X_j) . G_i          (float32 partial sums in LDS)
 //             dX_j   = sum_i conj(C_ij) . G_i  ->  dx_j = irdFFT(dX_j)
 // so no intermediate tensor ever reaches HBM.  Slot 0 of a packed spectrum holds
 // the two real bins Y_0 and Y_{p/2}; every product acts on them as two real
-// products (conjugation is the identity there).  The per-workgroup dC partial sums
-// are added into the caller's dc buffer with float32 atomics; a final in-place
-// irdFFT of dc (stream-ordered after this kernel) yields the time-domain gradient.
+// products (conjugation is the identity there).  The backward runs one wide persistent
+// workgroup per CU; its dC partial sums stay in LDS for all of its tiles and are then
+// added into the caller's dc buffer with float32 atomics (each workgroup starting at a
+// different offset); a final in-place irdFFT of dc (stream-ordered after the kernel)
+// yields the time-domain gradient.
 #include <hip/hip_runtime.h>
 
 #include "fft_device.hpp"
@@ -18,16 +20,17 @@
 
 namespace rdfft {
 
-constexpr int kBcaThreads = 256;
-constexpr int kBcaMaxAcc = 32;  // dC pair slots accumulated per thread
-
 template <int LOGN>
 struct BcaPlan {
   using P = RowPlan<LOGN>;
   static constexpr int N = P::N;
   static constexpr int TPR = P::TPR;
-  static_assert(TPR <= kBcaThreads, "row too long for the fused layer kernel");
-  static constexpr int NG = kBcaThreads / TPR;  // row groups per workgroup
+  static_assert(TPR <= 256, "row too long for the fused layer kernels");
+  // forward: 256 threads, or two row groups for the longest rows
+  static constexpr int FWD_WG = 2 * TPR > 256 ? 2 * TPR : 256;
+  // backward: one wide workgroup per CU keeps the number of dC partial sums (and so
+  // of atomics) small; 1024 threads when the plan is light on registers
+  static constexpr int BWD_WG = (P::E <= 8 && TPR <= 128) ? 1024 : 512;
   static constexpr int REGION = P::LDS_F2 > lds_padded_size(N) ? P::LDS_F2 : lds_padded_size(N);
 };
 
@@ -60,14 +63,14 @@ struct Acc<uint32_t> {
 extern __shared__ float2 bca_lds[];
 
 // x: [T][kb*N] pairs, c: [q][kb][N] pairs, y: [T][q*N] pairs (all in storage type Elem)
-template <int LOGN, class Elem>
-__global__ void __launch_bounds__(kBcaThreads) bca_forward_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
+template <int LOGN, class Elem, int WG = BcaPlan<LOGN>::FWD_WG>
+__global__ void __launch_bounds__(WG) bca_forward_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
                                                                   Elem* y, int64_t tokens, int q, int kb, int tt_per_tile,
                                                                   const float2* __restrict__ tw) {
   using B = BcaPlan<LOGN>;
   using In = typename Acc<Elem>::In;
   using Out = typename Acc<Elem>::Out;
-  constexpr int N = B::N, TPR = B::TPR, NG = B::NG, REG = B::REGION;
+  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
   const int tid = threadIdx.x;
   const int grp = tid / TPR, t = tid - grp * TPR;
   const int TT = tt_per_tile;
@@ -91,7 +94,7 @@ __global__ void __launch_bounds__(kBcaThreads) bca_forward_kernel(const Elem* __
 
   // Phase B: Y_i[k] = sum_j C_ij[k] . X_j[k]
   const In cin{c};
-  for (int e = tid; e < q * N; e += kBcaThreads) {
+  for (int e = tid; e < q * N; e += WG) {
     const int i = e / N, k = e - i * N;
     const bool s0 = k == 0;
     for (int tt = 0; tt < TT; ++tt) {
@@ -123,26 +126,26 @@ __global__ void __launch_bounds__(kBcaThreads) bca_forward_kernel(const Elem* __
 
 // gy: [T][q*N] pairs (read), dx: [T][kb*N] pairs (written; may alias gy when kb == q),
 // dc: [q][kb][N] float2 slots, receives the spectral partial sums (atomically)
-template <int LOGN, class Elem>
-__global__ void __launch_bounds__(kBcaThreads) bca_backward_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
+template <int LOGN, class Elem, int WG = BcaPlan<LOGN>::BWD_WG>
+__global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
                                                                    const Elem* gy, Elem* dx, float* __restrict__ dc,
                                                                    int64_t tokens, int q, int kb, int tt_per_tile,
                                                                    int64_t ntiles, const float2* __restrict__ tw) {
   using B = BcaPlan<LOGN>;
   using In = typename Acc<Elem>::In;
   using Out = typename Acc<Elem>::Out;
-  constexpr int N = B::N, TPR = B::TPR, NG = B::NG, REG = B::REGION;
+  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
   const int tid = threadIdx.x;
   const int grp = tid / TPR, t = tid - grp * TPR;
   const int TT = tt_per_tile;
   float2* const xs = bca_lds;                        // TT*kb regions: X, then dX
   float2* const gs = bca_lds + (size_t)TT * kb * REG;  // TT*q regions: G
   float2* const dummy = bca_lds + (size_t)TT * (kb + q) * REG;
+  float2* const acc = dummy + REG;                   // q*kb*N dC partial sums (pair slots)
   const int qkn = q * kb * N;
   const In cin{c};
 
-  float2 acc[kBcaMaxAcc];
-  static_for<kBcaMaxAcc>([&](auto uc) { acc[decltype(uc)::value] = make_float2(0.f, 0.f); });
+  for (int e = tid; e < qkn; e += WG) acc[e] = make_float2(0.f, 0.f);
 
   for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
     const int64_t tok0 = tile * TT;
@@ -172,28 +175,26 @@ __global__ void __launch_bounds__(kBcaThreads) bca_backward_kernel(const Elem* _
     }
     __syncthreads();
 
-    // Phase B1: dC_ij[k] += sum_t conj(X_tj[k]) . G_ti[k]
-    static_for<kBcaMaxAcc>([&](auto uc) {
-      constexpr int u = decltype(uc)::value;
-      const int e = tid + u * kBcaThreads;
-      if (e < qkn) {
-        const int k = e & (N - 1);
-        const int ij = e / N;
-        const int i = ij / kb, j = ij - i * kb;
-        const bool s0 = k == 0;
-        for (int tt = 0; tt < nvalid; ++tt) {
-          const float2 xv = xs[(size_t)(tt * kb + j) * REG + lds_pad(k)];
-          const float2 gv = gs[(size_t)(tt * q + i) * REG + lds_pad(k)];
-          const float2 pr = slot_cmul(xv, gv, s0);
-          acc[u].x += pr.x;
-          acc[u].y += pr.y;
-        }
+    // Phase B1: dC_ij[k] += sum_t conj(X_tj[k]) . G_ti[k]; each slot has one owner thread
+    for (int e = tid; e < qkn; e += WG) {
+      const int k = e & (N - 1);
+      const int ij = e / N;
+      const int i = ij / kb, j = ij - i * kb;
+      const bool s0 = k == 0;
+      float2 sum = acc[e];
+      for (int tt = 0; tt < nvalid; ++tt) {
+        const float2 xv = xs[(size_t)(tt * kb + j) * REG + lds_pad(k)];
+        const float2 gv = gs[(size_t)(tt * q + i) * REG + lds_pad(k)];
+        const float2 pr = slot_cmul(xv, gv, s0);
+        sum.x += pr.x;
+        sum.y += pr.y;
       }
-    });
+      acc[e] = sum;
+    }
     __syncthreads();
 
     // Phase B2: dX_j[k] = sum_i conj(C_ij[k]) . G_i[k], written over X_j
-    for (int e = tid; e < kb * N; e += kBcaThreads) {
+    for (int e = tid; e < kb * N; e += WG) {
       const int j = e / N, k = e - j * N;
       const bool s0 = k == 0;
       for (int tt = 0; tt < TT; ++tt) {
@@ -223,14 +224,17 @@ __global__ void __launch_bounds__(kBcaThreads) bca_backward_kernel(const Elem* _
     __syncthreads();
   }
 
-  static_for<kBcaMaxAcc>([&](auto uc) {
-    constexpr int u = decltype(uc)::value;
-    const int e = tid + u * kBcaThreads;
-    if (e < qkn) {
-      unsafeAtomicAdd(dc + 2 * (int64_t)e, acc[u].x);
-      unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, acc[u].y);
-    }
-  });
+  __syncthreads();
+  // fold this workgroup's partial sums into dc; workgroups start at different offsets
+  // so that they do not all contend for the same addresses at once
+  const int shift = (int)(((unsigned)blockIdx.x * 2654435761u) % (unsigned)((qkn + WG - 1) / WG)) * WG;
+  for (int e0 = tid; e0 < qkn; e0 += WG) {
+    int e = e0 + shift;
+    if (e >= qkn) e -= qkn;
+    const float2 v = acc[e];
+    unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
+    unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
+  }
 }
 
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
@@ -250,19 +254,37 @@ static int region_bytes(int logn) {
   return sizes[logn] * (int)sizeof(float2);
 }
 
-constexpr int kBcaMaxLogN = 12;      // p <= 8192
+constexpr int kBcaMaxLogN = 12;        // p <= 8192
 constexpr int kLdsLimit = 160 * 1024;  // gfx950 LDS per workgroup
-constexpr int kLdsTarget = 64 * 1024;  // aim for two workgroups per CU
+constexpr int kFwdLdsTarget = 64 * 1024;  // forward: aim for two workgroups per CU
 
-// tokens per tile so that a tile's spectra fit the LDS target; 0 if one token does not fit
-static int tokens_per_tile(int logn, int segs_per_token, int64_t tokens) {
+template <int LOGN>
+static int fwd_wg() { return BcaPlan<LOGN>::FWD_WG; }
+static int bwd_wg(int logn) {
+  static const int wg[kBcaMaxLogN + 1] = {
+      BcaPlan<0>::BWD_WG, BcaPlan<1>::BWD_WG, BcaPlan<2>::BWD_WG,  BcaPlan<3>::BWD_WG,  BcaPlan<4>::BWD_WG,
+      BcaPlan<5>::BWD_WG, BcaPlan<6>::BWD_WG, BcaPlan<7>::BWD_WG,  BcaPlan<8>::BWD_WG,  BcaPlan<9>::BWD_WG,
+      BcaPlan<10>::BWD_WG, BcaPlan<11>::BWD_WG, BcaPlan<12>::BWD_WG};
+  return wg[logn];
+}
+static int tpr_of(int logn) {
+  static const int tpr[kBcaMaxLogN + 1] = {
+      BcaPlan<0>::TPR, BcaPlan<1>::TPR, BcaPlan<2>::TPR, BcaPlan<3>::TPR,  BcaPlan<4>::TPR,  BcaPlan<5>::TPR,
+      BcaPlan<6>::TPR, BcaPlan<7>::TPR, BcaPlan<8>::TPR, BcaPlan<9>::TPR, BcaPlan<10>::TPR, BcaPlan<11>::TPR,
+      BcaPlan<12>::TPR};
+  return tpr[logn];
+}
+
+// Tokens per tile: a tile's spectra plus one spare region must fit the LDS budget; the
+// tile is grown until every row group has a transform in the output phase.  0 when a
+// single token does not fit.
+static int tokens_per_tile(int logn, int kb, int q, int64_t tokens, int wg, int budget) {
   const int rb = region_bytes(logn);
-  const int64_t per_tok = (int64_t)segs_per_token * rb;
-  if (per_tok + rb > kLdsLimit) return 0;
-  int64_t tt = (kLdsTarget - rb) / per_tok;
-  if (tt < 1) tt = 1;
-  if (tt > tokens) tt = tokens;
-  if (tt < 1) tt = 1;
+  const int64_t per_tok = (int64_t)(kb + q) * rb;
+  if (per_tok + rb > budget) return 0;
+  const int ng = wg / tpr_of(logn);
+  int64_t tt = 1;
+  while ((tt + 1) * per_tok + rb <= budget && tt * kb < ng && tt < tokens && tt < 64) ++tt;
   return (int)tt;
 }
 
@@ -274,29 +296,36 @@ static hipError_t set_lds_limit(K kernel) {
 
 template <int LOGN, class Elem>
 static hipError_t fwd_impl(const BcaArgs& a, const float2* tw, hipStream_t stream) {
-  const int TT = tokens_per_tile(LOGN, a.kb + a.q, a.tokens);
+  constexpr int WG = BcaPlan<LOGN>::FWD_WG;
+  const int TT = tokens_per_tile(LOGN, a.kb, a.q, a.tokens, WG, std::max(kFwdLdsTarget, 3 * region_bytes(LOGN)));
   if (TT == 0) return hipErrorInvalidValue;
   const size_t lds = (size_t)(TT * (a.kb + a.q) + 1) * region_bytes(LOGN);
   static const hipError_t attr = set_lds_limit(bca_forward_kernel<LOGN, Elem>);
   if (attr != hipSuccess) return attr;
   const int64_t tiles = (a.tokens + TT - 1) / TT;
-  hipLaunchKernelGGL((bca_forward_kernel<LOGN, Elem>), dim3((unsigned)tiles), dim3(kBcaThreads), lds, stream,
+  hipLaunchKernelGGL((bca_forward_kernel<LOGN, Elem>), dim3((unsigned)tiles), dim3(WG), lds, stream,
                      static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<Elem*>(a.y), a.tokens,
                      a.q, a.kb, TT, tw);
   return hipGetLastError();
 }
 
+// LDS of the backward's dC partial sums: q*kb*p/2 pair slots of float2
+static int64_t dc_lds_bytes(int logn, int q, int kb) { return (int64_t)q * kb * ((int64_t)1 << logn) * 8; }
+
 template <int LOGN, class Elem>
 static hipError_t bwd_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
-  const int TT = tokens_per_tile(LOGN, a.kb + a.q, a.tokens);
+  constexpr int WG = BcaPlan<LOGN>::BWD_WG;
+  const int64_t acc_bytes = dc_lds_bytes(LOGN, a.q, a.kb);
+  const int TT = tokens_per_tile(LOGN, a.kb, a.q, a.tokens, WG, kLdsLimit - (int)acc_bytes);
   if (TT == 0) return hipErrorInvalidValue;
-  const size_t lds = (size_t)(TT * (a.kb + a.q) + 1) * region_bytes(LOGN);
+  const size_t lds = (size_t)(TT * (a.kb + a.q) + 1) * region_bytes(LOGN) + (size_t)acc_bytes;
   static const hipError_t attr = set_lds_limit(bca_backward_kernel<LOGN, Elem>);
   if (attr != hipSuccess) return attr;
   const int64_t tiles = (a.tokens + TT - 1) / TT;
-  const int per_cu = lds <= (size_t)kLdsTarget ? 2 : 1;
+  // persistent workgroups, as many as fit at once: fewer workgroups, fewer dC partials
+  const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / WG));
   const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
-  hipLaunchKernelGGL((bca_backward_kernel<LOGN, Elem>), dim3((unsigned)grid), dim3(kBcaThreads), lds, stream,
+  hipLaunchKernelGGL((bca_backward_kernel<LOGN, Elem>), dim3((unsigned)grid), dim3(WG), lds, stream,
                      static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<const Elem*>(a.y),
                      static_cast<Elem*>(a.dx), a.dc, a.tokens, a.q, a.kb, TT, tiles, tw);
   return hipGetLastError();
@@ -314,11 +343,13 @@ static std::array<BcaBwdFn, sizeof...(L)> bwd_table(bool bf16, std::integer_sequ
   return {(bf16 ? &bwd_impl<L, uint32_t> : &bwd_impl<L, float2>)...};
 }
 
-bool bca_shape_supported(int logp, int q, int kb) {
+bool bca_shape_supported(int logp, int q, int kb, bool backward) {
   const int logn = logp - 1;
   if (logn < 0 || logn > kBcaMaxLogN) return false;
-  if ((int64_t)q * kb * (1 << logn) > (int64_t)kBcaThreads * kBcaMaxAcc) return false;
-  return tokens_per_tile(logn, kb + q, 1) > 0;
+  // the backward keeps q*kb*p/2 dC pair slots in LDS next to one token's spectra
+  const int64_t extra = backward ? dc_lds_bytes(logn, q, kb) : 0;
+  if (extra >= kLdsLimit) return false;
+  return tokens_per_tile(logn, kb, q, 1, 256, kLdsLimit - (int)extra) > 0;
 }
 
 hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream) {

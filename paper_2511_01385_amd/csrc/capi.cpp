@@ -108,7 +108,7 @@ struct BcaShape {
 };
 
 int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t d_out, int64_t p, int64_t tokens,
-              int dtype, BcaShape* sh) {
+              int dtype, bool backward, BcaShape* sh) {
   if (dtype != RDFFT_F32 && dtype != RDFFT_BF16) return RDFFT_EINVAL;
   if (tokens < 0 || d_in <= 0 || d_out <= 0 || p <= 0) return RDFFT_EINVAL;
   if (p < 2 || (p & 1)) return RDFFT_EINVAL;
@@ -119,7 +119,7 @@ int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t
   sh->q = (int)q;
   sh->kb = (int)kb;
   sh->logp = ilog2(p);
-  if (!rdfft::bca_shape_supported(sh->logp, sh->q, sh->kb)) return RDFFT_EUNSUPPORTED;
+  if (!rdfft::bca_shape_supported(sh->logp, sh->q, sh->kb, backward)) return RDFFT_EUNSUPPORTED;
   const int s = elem_bytes(dtype);
   int64_t t = 0;
   if (!mul_ok(tokens, d_in, &t) || !mul_ok(t, s, &sh->x_bytes)) return RDFFT_EINVAL;
@@ -150,7 +150,7 @@ int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grad
                 int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream) {
   if (grads != nullptr) return RDFFT_EINVAL;
   BcaShape sh;
-  int st = check_bca(x, c_spectra, y, d_in, d_out, p, tokens, dtype, &sh);
+  int st = check_bca(x, c_spectra, y, d_in, d_out, p, tokens, dtype, false, &sh);
   if (st != RDFFT_OK) return st;
   if (tokens == 0) return RDFFT_OK;
   // y may be x itself (an in-place layer) only when the shapes agree
@@ -171,7 +171,7 @@ int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* gr
                  int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream) {
   if (grads == nullptr) return RDFFT_EINVAL;
   BcaShape sh;
-  int st = check_bca(x, c_spectra, gy, d_in, d_out, p, tokens, dtype, &sh);
+  int st = check_bca(x, c_spectra, gy, d_in, d_out, p, tokens, dtype, true, &sh);
   if (st != RDFFT_OK) return st;
   float* dc = grads->dc;
   void* dx = grads->dx;

@@ -32,7 +32,7 @@ hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t st
 // also zeroes dc first and transforms it to the time domain afterwards
 hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu);
 
-// whether the fused kernels handle p = 2^logp with q x kb blocks
-bool bca_shape_supported(int logp, int q, int kb);
+// whether the fused forward (or backward) kernel handles p = 2^logp with q x kb blocks
+bool bca_shape_supported(int logp, int q, int kb, bool backward);
 
 }  // namespace rdfft
