@@ -34,17 +34,13 @@ struct BcaPlan {
   static constexpr int REGION = P::LDS_F2 > lds_padded_size(N) ? P::LDS_F2 : lds_padded_size(N);
 };
 
-// a . b on packed pair slots (slot 0 = two real bins)
-__device__ __forceinline__ float2 slot_mul(float2 a, float2 b, bool slot0) {
-  const float re = slot0 ? a.x * b.x : fmaf(a.x, b.x, -a.y * b.y);
-  const float im = slot0 ? a.y * b.y : fmaf(a.x, b.y, a.y * b.x);
-  return make_float2(re, im);
-}
-// conj(a) . b on packed pair slots
-__device__ __forceinline__ float2 slot_cmul(float2 a, float2 b, bool slot0) {
-  const float re = slot0 ? a.x * b.x : fmaf(a.x, b.x, a.y * b.y);
-  const float im = slot0 ? a.y * b.y : fmaf(a.x, b.y, -a.y * b.x);
-  return make_float2(re, im);
+// acc + a.b (or acc + conj(a).b) on packed pair slots.  Slot 0 (S0) holds the two real
+// bins Y_0 and Y_{p/2}: there the product is two real products and conj is the identity.
+template <bool S0, bool CONJ>
+__device__ __forceinline__ float2 slot_mac(float2 acc, float2 a, float2 b) {
+  if constexpr (S0) return make_float2(fmaf(a.x, b.x, acc.x), fmaf(a.y, b.y, acc.y));
+  if constexpr (!CONJ) return make_float2(fmaf(a.x, b.x, fmaf(-a.y, b.y, acc.x)), fmaf(a.x, b.y, fmaf(a.y, b.x, acc.y)));
+  return make_float2(fmaf(a.x, b.x, fmaf(a.y, b.y, acc.x)), fmaf(a.x, b.y, fmaf(-a.y, b.x, acc.y)));
 }
 
 template <class Elem>
@@ -92,22 +88,27 @@ __global__ void __launch_bounds__(WG) bca_forward_kernel(const Elem* __restrict_
   }
   __syncthreads();
 
-  // Phase B: Y_i[k] = sum_j C_ij[k] . X_j[k]
+  // Phase B: Y_i[k] = sum_j C_ij[k] . X_j[k]; a thread takes one (token, bin) and all i, j.
+  // Bin 0 is slot 0 and takes the branch with real products (one lane of one wave).
   const In cin{c};
-  for (int e = tid; e < q * N; e += WG) {
-    const int i = e / N, k = e - i * N;
-    const bool s0 = k == 0;
-    for (int tt = 0; tt < TT; ++tt) {
-      float2 acc = make_float2(0.f, 0.f);
-      for (int j = 0; j < kb; ++j) {
-        const float2 cv = cin.load((i * kb + j) * N + k);
-        const float2 xv = xs[(size_t)(tt * kb + j) * REG + lds_pad(k)];
-        const float2 pr = slot_mul(cv, xv, s0);
-        acc.x += pr.x;
-        acc.y += pr.y;
+  for (int it = tid; it < TT * N; it += WG) {
+    const int tt = it / N, k = it - tt * N;
+    const float2* xk = xs + (size_t)tt * kb * REG + lds_pad(k);
+    float2* yk = ys + (size_t)tt * q * REG + lds_pad(k);
+    auto block_sum = [&](auto s0c) {
+      constexpr bool S0 = decltype(s0c)::value;
+      int ci = k;  // pair index of C_ij[k] = (i*kb + j)*N + k
+      for (int i = 0; i < q; ++i) {
+        float2 a = make_float2(0.f, 0.f);
+        // unrolled so that several L2 loads of C are in flight at once
+#pragma unroll 4
+        for (int j = 0; j < kb; ++j) a = slot_mac<S0, false>(a, cin.load(ci + j * N), xk[j * REG]);
+        ci += kb * N;
+        yk[i * REG] = a;
       }
-      ys[(size_t)(tt * q + i) * REG + lds_pad(k)] = acc;
-    }
+    };
+    if (k == 0) block_sum(std::true_type{});
+    else block_sum(std::false_type{});
   }
   __syncthreads();
 
@@ -180,34 +181,37 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
       const int k = e & (N - 1);
       const int ij = e / N;
       const int i = ij / kb, j = ij - i * kb;
-      const bool s0 = k == 0;
-      float2 sum = acc[e];
-      for (int tt = 0; tt < nvalid; ++tt) {
-        const float2 xv = xs[(size_t)(tt * kb + j) * REG + lds_pad(k)];
-        const float2 gv = gs[(size_t)(tt * q + i) * REG + lds_pad(k)];
-        const float2 pr = slot_cmul(xv, gv, s0);
-        sum.x += pr.x;
-        sum.y += pr.y;
-      }
-      acc[e] = sum;
+      const float2* xp = xs + (size_t)j * REG + lds_pad(k);
+      const float2* gp = gs + (size_t)i * REG + lds_pad(k);
+      auto contract = [&](auto s0c) {
+        constexpr bool S0 = decltype(s0c)::value;
+        float2 sum = acc[e];
+#pragma unroll 4
+        for (int tt = 0; tt < nvalid; ++tt) sum = slot_mac<S0, true>(sum, xp[(size_t)tt * kb * REG], gp[(size_t)tt * q * REG]);
+        acc[e] = sum;
+      };
+      if (k == 0) contract(std::true_type{});
+      else contract(std::false_type{});
     }
     __syncthreads();
 
     // Phase B2: dX_j[k] = sum_i conj(C_ij[k]) . G_i[k], written over X_j
-    for (int e = tid; e < kb * N; e += WG) {
-      const int j = e / N, k = e - j * N;
-      const bool s0 = k == 0;
-      for (int tt = 0; tt < TT; ++tt) {
-        float2 sum = make_float2(0.f, 0.f);
-        for (int i = 0; i < q; ++i) {
-          const float2 cv = cin.load((i * kb + j) * N + k);
-          const float2 gv = gs[(size_t)(tt * q + i) * REG + lds_pad(k)];
-          const float2 pr = slot_cmul(cv, gv, s0);
-          sum.x += pr.x;
-          sum.y += pr.y;
+    for (int it = tid; it < TT * N; it += WG) {
+      const int tt = it / N, k = it - tt * N;
+      const float2* gk = gs + (size_t)tt * q * REG + lds_pad(k);
+      float2* xk = xs + (size_t)tt * kb * REG + lds_pad(k);
+      auto grad_x = [&](auto s0c) {
+        constexpr bool S0 = decltype(s0c)::value;
+        for (int j = 0; j < kb; ++j) {
+          float2 a = make_float2(0.f, 0.f);
+          const int ci = j * N + k;  // pair index of C_0j[k]; C_ij[k] is i*kb*N further
+#pragma unroll 4
+          for (int i = 0; i < q; ++i) a = slot_mac<S0, true>(a, cin.load(ci + i * kb * N), gk[i * REG]);
+          xk[j * REG] = a;
         }
-        xs[(size_t)(tt * kb + j) * REG + lds_pad(k)] = sum;
-      }
+      };
+      if (k == 0) grad_x(std::true_type{});
+      else grad_x(std::false_type{});
     }
     __syncthreads();
 

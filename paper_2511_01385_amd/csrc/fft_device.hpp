@@ -205,6 +205,22 @@ struct LdsSpectrum {
 // multiple of 16), so one padded base per butterfly plus compile-time offsets suffices.
 constexpr int pad_step(int d) { return d + (d >> 4); }
 
+// Synchronises the TPR threads that share one row's LDS region.  When the row lives
+// inside one wavefront (TPR divides 64) no workgroup barrier is needed: all LDS
+// operations of a CU are performed wavefront-wide in one global order, so a wave's
+// later LDS reads observe its earlier LDS writes, and only compiler code motion has to
+// be stopped.  Rows spanning several waves use the workgroup barrier.
+template <int TPR>
+__device__ __forceinline__ void row_sync() {
+  if constexpr (TPR <= 64) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  } else {
+    __syncthreads();
+  }
+}
+
 // ----------------------------------------------------------------------------------
 template <int LOGN>
 struct RowPlan {
@@ -271,7 +287,7 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
         });
       }
     });
-    __syncthreads();
+    row_sync<TPR>();
     static_for<BPT2>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int pg = lds_pad(t + b * TPR);
@@ -281,7 +297,7 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
         if constexpr (r / (R2 / C) == c) nv[b * R2 + r] = lds[pg + pad_step((r - c * (R2 / C)) * (N / R2))];
       });
     });
-    __syncthreads();
+    row_sync<TPR>();
   });
   static_for<E>([&](auto ic) { v[decltype(ic)::value] = nv[decltype(ic)::value]; });
 }
@@ -311,7 +327,7 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
   if constexpr (LOGN == 0) {
     // n = 2: Y_0 = x0 + x1, Y_1 = x0 - x1.  The barrier stays outside any branch.
     const float2 z = src.load(0);
-    if constexpr (DST_IN_LDS) __syncthreads();
+    if constexpr (DST_IN_LDS) row_sync<TPR>();
     if (active) dst.store(0, make_float2(z.x + z.y, z.x - z.y));
     return;
   } else {
@@ -349,7 +365,7 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
           }
         });
       });
-      if constexpr (DST_IN_LDS) __syncthreads();
+      if constexpr (DST_IN_LDS) row_sync<TPR>();
     } else {
       static_for<BPL>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
@@ -359,7 +375,7 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
           lds[pg + pad_step(r * NsL)] = v[b * RL + r + RL / 2];
         });
       });
-      __syncthreads();
+      row_sync<TPR>();
       static_for<BPL>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
         const int g = t + b * TPR;
@@ -375,7 +391,7 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
           }
         });
       });
-      if constexpr (DST_IN_LDS) __syncthreads();
+      if constexpr (DST_IN_LDS) row_sync<TPR>();
     }
     if (!active) return;
     static_for<BPL>([&](auto bc) {
@@ -471,7 +487,7 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
         });
       });
     } else {
-      if constexpr (SRC_IN_LDS) __syncthreads();
+      if constexpr (SRC_IN_LDS) row_sync<TPR>();
       constexpr int S0 = N / R0;
       static_for<BPT0>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
@@ -490,7 +506,7 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
       });
       // element m = N/2 (thread 0) reads index 0, which no mirror write touches
       if (t == 0) lds[0] = zhalf;
-      __syncthreads();
+      row_sync<TPR>();
       static_for<BPT0>([&](auto bc) {
         constexpr int b = decltype(bc)::value;
         const int g = t + b * TPR;
@@ -500,7 +516,7 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
           v[b * R0 + r + R0 / 2] = lds[pg + pad_step(r * S0)];
         });
       });
-      __syncthreads();
+      row_sync<TPR>();
     }
     stockham_from<LOGN, 0, true>(v, t, lds, tw);
     if (!active) return;
