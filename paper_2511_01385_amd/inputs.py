@@ -44,11 +44,12 @@ def generator(seed: int) -> np.random.Generator:
 
 
 def _f32_to_bf16_bits(a32: np.ndarray) -> np.ndarray:
-    u = np.ascontiguousarray(a32, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    nan = (u & 0x7FFFFFFF) > 0x7F800000
-    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
-    out = rounded.astype(np.uint16)
-    out[nan] = ((u[nan] >> 16) | 0x40).astype(np.uint16)  # keep NaNs quiet NaNs
+    u = np.ascontiguousarray(a32, dtype=np.float32).view(np.uint32)
+    # no wrap-around for finite values and infinities (u <= 0xFF800000)
+    out = ((u + np.uint32(0x7FFF) + ((u >> 16) & np.uint32(1))) >> 16).astype(np.uint16)
+    nan = (u & np.uint32(0x7FFFFFFF)) > np.uint32(0x7F800000)
+    if nan.any():
+        out[nan] = ((u[nan] >> 16) | 0x40).astype(np.uint16)  # keep NaNs quiet NaNs
     return out
 
 
@@ -73,9 +74,20 @@ def to_f64(stored: np.ndarray, dtype: str) -> np.ndarray:
 
 
 def normal_rows(seed: int, rows: int, n: int, dtype: str, sigma: float = 1.0) -> np.ndarray:
-    """(rows, n) storage array with entries ~ N(0, sigma^2)."""
+    """(rows, n) storage array with entries ~ N(0, sigma^2).
+
+    Drawn in row-major order from one PCG64 stream, a block of rows at a time
+    (the stream is consumed in the same order as by a single draw).
+    """
+    if dtype not in ("f32", "bf16"):
+        raise ValueError(dtype)
     g = generator(seed)
-    return round_to(g.standard_normal((rows, n)) * sigma, dtype)
+    out = np.empty((rows, n), dtype=np.float32 if dtype == "f32" else np.uint16)
+    step = max(1, (1 << 20) // max(n, 1))
+    for r0 in range(0, rows, step):
+        r1 = min(rows, r0 + step)
+        out[r0:r1] = round_to(g.standard_normal((r1 - r0, n)) * sigma, dtype)
+    return out
 
 
 def circulant_spectra(rng: np.random.Generator, q: int, kb: int, p: int, sigma: float, dtype: str):
