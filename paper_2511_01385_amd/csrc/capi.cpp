@@ -95,10 +95,11 @@ int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stre
   int st = check_transform(buf, rows, n, dtype);
   if (st != RDFFT_OK || rows == 0) return st;
   const float2* tw = nullptr;
-  st = ensure_device(&tw, nullptr);
+  int num_cu = 0;
+  st = ensure_device(&tw, &num_cu);
   if (st != RDFFT_OK) return st;
   const hipError_t e = rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype == RDFFT_BF16, inv, tw,
-                                                reinterpret_cast<hipStream_t>(stream));
+                                                reinterpret_cast<hipStream_t>(stream), num_cu);
   return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
 }
 

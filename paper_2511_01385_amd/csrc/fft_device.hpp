@@ -158,9 +158,14 @@ struct Dft<32, INV> {
 };
 
 // ----------------------------------------------------------------------------------
-// Row storage accessors (complex-pair indexed).
+// Row storage accessors (complex-pair indexed).  load_raw fetches a slot in its storage
+// form and widen turns that into float2, so a caller can issue a row's loads early and
+// widen them when it computes; load(m) == widen(load_raw(m)).
 struct GlobalF32 {
+  using raw_t = float2;
   float2* base;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return r; }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return base[m]; }
   __device__ __forceinline__ void store(int m, float2 v) const { base[m] = v; }
 };
@@ -177,24 +182,36 @@ __device__ __forceinline__ uint32_t f32_to_bf16x2(float2 v) {  // round to neare
 }
 
 struct GlobalBF16 {
+  using raw_t = uint32_t;
   uint32_t* base;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return bf16x2_to_f32(r); }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return bf16x2_to_f32(base[m]); }
   __device__ __forceinline__ void store(int m, float2 v) const { base[m] = f32_to_bf16x2(v); }
 };
 
 // Read-only views (inputs that must never be written)
 struct ConstF32 {
+  using raw_t = float2;
   const float2* base;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return r; }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return base[m]; }
 };
 struct ConstBF16 {
+  using raw_t = uint32_t;
   const uint32_t* base;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return bf16x2_to_f32(r); }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return bf16x2_to_f32(base[m]); }
 };
 
 // A packed spectrum kept in a row's (padded) LDS region
 struct LdsSpectrum {
+  using raw_t = float2;
   float2* base;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return r; }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return base[lds_pad(m)]; }
   __device__ __forceinline__ float2 load(int m) const { return base[lds_pad(m)]; }
   __device__ __forceinline__ void store(int m, float2 v) const { base[lds_pad(m)] = v; }
 };
@@ -246,14 +263,25 @@ __device__ __forceinline__ void stockham_compute(float2* v, int t, const float2*
   constexpr int BPT = P::E / R;
   if constexpr (Q > 0) {
     constexpr int kOff = pass_table_offset(LOGN, Q);  // forced to a compile-time constant
-    const float2* __restrict__ twq = tw + kOff;
+    constexpr int L = tw_loaded(R);
+    static_assert(kOff % 2 == 0 && L % 2 == 0, "twiddle pairs must be 16-byte aligned");
+    const float4* __restrict__ twq = reinterpret_cast<const float4*>(tw + kOff);
     static_for<BPT>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * P::TPR;
       const int k = g & (Ns - 1);
+      // w[r] = W_{Ns*R}^{r*k}: the stored powers r <= L, then w[r] = w[r - L] * w[L]
+      float2 w[R > L ? R : L + 1];
+      static_for<L / 2>([&](auto ic) {
+        constexpr int i = decltype(ic)::value;
+        const float4 pr = twq[k * (L / 2) + i];
+        w[2 * i + 1] = make_float2(pr.x, pr.y);
+        w[2 * i + 2] = make_float2(pr.z, pr.w);
+      });
       static_for<R - 1>([&](auto rc) {
         constexpr int r = decltype(rc)::value + 1;
-        v[b * R + r] = c_mul<INV>(v[b * R + r], twq[(r - 1) * Ns + k]);
+        if constexpr (r > L) w[r] = c_mul<false>(w[r - L], w[L]);
+        v[b * R + r] = c_mul<INV>(v[b * R + r], w[r]);
       });
     });
   }
@@ -312,37 +340,49 @@ __device__ __forceinline__ void stockham_from(float2* v, int t, float2* lds, con
 }
 
 // ----------------------------------------------------------------------------------
-// Forward rdFFT of one row.
+// Forward rdFFT of one row, in two steps so that a caller can issue the loads of one
+// row before it computes another:
+//   load_forward        thread t's first-pass inputs in storage form: slot
+//                       g + r*(N/R0) at raw[b*R0 + r], g = t + b*TPR
+//   row_forward_loaded  the transform of those inputs
 //   t      thread index within the row's TPR threads
-//   active false for padding rows past the end of the batch (no global access)
-//   src    input pairs (x_{2m}, x_{2m+1}), m < N
+//   active false for padding rows past the end of the batch: their loads read a valid
+//          row and their results are not stored
 //   dst    output packed pairs P[k]
 //   lds    the row's LDS region (RowPlan::LDS_F2 float2); may be the storage of dst
 //          when DST_IN_LDS (then a barrier separates the last LDS read from the stores)
-template <int LOGN, bool DST_IN_LDS, class Src, class Dst>
-__device__ __forceinline__ void row_forward(int t, bool active, const Src& src, const Dst& dst, float2* lds,
-                                            const float2* __restrict__ tw) {
+template <int LOGN, class Src>
+__device__ __forceinline__ void load_forward(int t, const Src& src, typename Src::raw_t* raw) {
   using P = RowPlan<LOGN>;
-  constexpr int N = P::N, E = P::E, TPR = P::TPR;
   if constexpr (LOGN == 0) {
-    // n = 2: Y_0 = x0 + x1, Y_1 = x0 - x1.  The barrier stays outside any branch.
-    const float2 z = src.load(0);
-    if constexpr (DST_IN_LDS) row_sync<TPR>();
-    if (active) dst.store(0, make_float2(z.x + z.y, z.x - z.y));
-    return;
+    raw[0] = src.load_raw(0);
   } else {
-    float2 v[E];
-    constexpr int R0 = radix(LOGN, 0), BPT0 = E / R0;
+    constexpr int N = P::N, E = P::E, TPR = P::TPR, R0 = radix(LOGN, 0), BPT0 = E / R0;
     static_for<BPT0>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * TPR;
       static_for<R0>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
-        // unconditional: inactive rows point at a valid row, so the loads stay in
-        // bounds and all of them are in flight at once
-        v[b * R0 + r] = src.load(g + r * (N / R0));
+        raw[b * R0 + r] = src.load_raw(g + r * (N / R0));
       });
     });
+  }
+}
+
+template <int LOGN, bool DST_IN_LDS, class Src, class Dst>
+__device__ __forceinline__ void row_forward_loaded(int t, bool active, const typename Src::raw_t* raw,
+                                                   const Dst& dst, float2* lds, const float2* __restrict__ tw) {
+  using P = RowPlan<LOGN>;
+  constexpr int N = P::N, E = P::E, TPR = P::TPR;
+  if constexpr (LOGN == 0) {
+    // n = 2: Y_0 = x0 + x1, Y_1 = x0 - x1.  The barrier stays outside any branch.
+    const float2 z = Src::widen(raw[0]);
+    if constexpr (DST_IN_LDS) row_sync<TPR>();
+    if (active) dst.store(0, make_float2(z.x + z.y, z.x - z.y));
+    return;
+  } else {
+    float2 v[E];
+    static_for<E>([&](auto ic) { v[decltype(ic)::value] = Src::widen(raw[decltype(ic)::value]); });
     stockham_from<LOGN, 0, false>(v, t, lds, tw);
 
     // Post-pass.  After the last pass thread t holds Z_m at m = g_b + r*(N/RL).
@@ -397,15 +437,16 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
     static_for<BPL>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * TPR;
+      const float2 twg = twp[g];  // -i W_n^g / 2
       static_for<RL / 2>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
         const int k = g + r * NsL;
         const float2 a = v[b * RL + r];
         const float2 bc2 = c_conj(partner[b * (RL / 2) + r]);
         const float2 s = c_add(a, bc2), d = c_sub(a, bc2);
-        // Y_k = s/2 + (-i W_n^k / 2) d,  Y_{N-k} = conj(s/2 - (-i W_n^k / 2) d); the table holds
-        // -i W_n^k / 2 (k = 0 reads an entry whose result the slot-0 select replaces)
-        const float2 q = c_mul<false>(d, twp[k]);
+        // Y_k = s/2 + (-i W_n^k / 2) d,  Y_{N-k} = conj(s/2 - (-i W_n^k / 2) d), with
+        // W_n^k = W_n^g W_{2RL}^r (k = 0: the slot-0 select replaces the result)
+        const float2 q = c_mul<false>(d, rot<2 * RL, r, false>(twg));
         float2 lo = make_float2(fmaf(s.x, 0.5f, q.x), fmaf(s.y, 0.5f, q.y));
         float2 hi = make_float2(fmaf(s.x, 0.5f, -q.x), -fmaf(s.y, 0.5f, -q.y));
         int hi_idx = N - k;
@@ -425,18 +466,53 @@ __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, 
   }
 }
 
-// ----------------------------------------------------------------------------------
-// Inverse rdFFT of one row: packed pairs P[k] (src) -> pairs (x_{2m}, x_{2m+1}) (dst).
-// SRC_IN_LDS: src lives in this row's LDS region (a barrier then separates its reads
-// from the first LDS write).
-template <int LOGN, bool SRC_IN_LDS, class Src, class Dst>
-__device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, const Dst& dst, float2* lds,
+template <int LOGN, bool DST_IN_LDS, class Src, class Dst>
+__device__ __forceinline__ void row_forward(int t, bool active, const Src& src, const Dst& dst, float2* lds,
                                             const float2* __restrict__ tw) {
+  typename Src::raw_t raw[RowPlan<LOGN>::E];
+  load_forward<LOGN>(t, src, raw);
+  row_forward_loaded<LOGN, DST_IN_LDS, Src>(t, active, raw, dst, lds, tw);
+}
+
+// ----------------------------------------------------------------------------------
+// Inverse rdFFT of one row: packed pairs P[k] -> pairs (x_{2m}, x_{2m+1}) (dst), split
+// like the forward:
+//   load_inverse        thread t's pre-pass inputs in storage form: for m = g + r*(N/R0),
+//                       r < R0/2, slot m at raw[b*R0 + r] and its partner N - m (N/2 for
+//                       m == 0) at raw[b*R0 + R0/2 + r]
+//   row_inverse_loaded  the transform of those inputs
+// SRC_IN_LDS: the loads read this row's LDS region (a barrier then separates them from
+// the first LDS write).
+template <int LOGN, class Src>
+__device__ __forceinline__ void load_inverse(int t, const Src& src, typename Src::raw_t* raw) {
+  using P = RowPlan<LOGN>;
+  if constexpr (LOGN == 0) {
+    raw[0] = src.load_raw(0);
+  } else {
+    constexpr int N = P::N, E = P::E, TPR = P::TPR, R0 = radix(LOGN, 0), BPT0 = E / R0;
+    static_for<BPT0>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int g = t + b * TPR;
+      static_for<R0 / 2>([&](auto rc) {
+        constexpr int r = decltype(rc)::value;
+        const int m = g + r * (N / R0);
+        // m == 0 only for thread 0 at (b, r) = (0, 0); it pairs with slot N/2 instead of N
+        const bool z = (b == 0 && r == 0) ? (t == 0) : false;
+        raw[b * R0 + r] = src.load_raw(m);
+        raw[b * R0 + R0 / 2 + r] = src.load_raw(z ? N / 2 : N - m);
+      });
+    });
+  }
+}
+
+template <int LOGN, bool SRC_IN_LDS, class Src, class Dst>
+__device__ __forceinline__ void row_inverse_loaded(int t, bool active, const typename Src::raw_t* raw,
+                                                   const Dst& dst, float2* lds, const float2* __restrict__ tw) {
   using P = RowPlan<LOGN>;
   constexpr int N = P::N, E = P::E, TPR = P::TPR;
   constexpr float sc = 1.0f / (2.0f * N);  // 1/n
   if constexpr (LOGN == 0) {
-    const float2 y = src.load(0);
+    const float2 y = Src::widen(raw[0]);
     if (active) dst.store(0, make_float2(0.5f * (y.x + y.y), 0.5f * (y.x - y.y)));
     return;
   } else {
@@ -449,18 +525,16 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
     static_for<BPT0>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * TPR;
+      const float2 twg = twp[N / 2 + g];  // i conj(W_n^g) / n
       static_for<R0 / 2>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
-        const int m = g + r * (N / R0);
-        // m == 0 only for thread 0 at (b, r) = (0, 0); it pairs with slot N/2 instead of N
         const bool z = (b == 0 && r == 0) ? (t == 0) : false;
-        const float2 ya = src.load(m);
-        const float2 yraw = src.load(z ? N / 2 : N - m);
-        const float2 yb = c_conj(yraw);
+        const float2 ya = Src::widen(raw[b * R0 + r]);
+        const float2 yb = c_conj(Src::widen(raw[b * R0 + R0 / 2 + r]));
         const float2 s = c_add(ya, yb), d = c_sub(ya, yb);
-        // Z~_m = (s + i conj(W_n^m) d) / n,  Z~_{N-m} = conj(s - i conj(W_n^m) d) / n; the table
-        // holds i conj(W_n^m) / n
-        const float2 q = c_mul<false>(d, twp[N / 2 + m]);
+        // Z~_m = (s + i conj(W_n^m) d) / n,  Z~_{N-m} = conj(s - i conj(W_n^m) d) / n for
+        // m = g + r*N/R0, with conj(W_n^m) = conj(W_n^g) conj(W_{2R0}^r)
+        const float2 q = c_mul<false>(d, rot<2 * R0, r, true>(twg));
         float2 lo = make_float2(fmaf(s.x, sc, q.x), fmaf(s.y, sc, q.y));
         float2 hi = make_float2(fmaf(s.x, sc, -q.x), -fmaf(s.y, sc, -q.y));
         if constexpr (b == 0 && r == 0) {
@@ -530,6 +604,14 @@ __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, 
       });
     });
   }
+}
+
+template <int LOGN, bool SRC_IN_LDS, class Src, class Dst>
+__device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, const Dst& dst, float2* lds,
+                                            const float2* __restrict__ tw) {
+  typename Src::raw_t raw[RowPlan<LOGN>::E];
+  load_inverse<LOGN>(t, src, raw);
+  row_inverse_loaded<LOGN, SRC_IN_LDS, Src>(t, active, raw, dst, lds, tw);
 }
 
 }  // namespace rdfft

@@ -10,9 +10,10 @@
 
 namespace rdfft {
 
-// In-place forward (inv = false) or inverse rdFFT of `rows` rows of 2^(logn+1) elements.
+// In-place forward (inv = false) or inverse rdFFT of `rows` rows of 2^(logn+1) elements
+// (rows >= 1); num_cu sizes the persistent grid.
 hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, bool bf16, bool inv, const float2* tw,
-                             hipStream_t stream);
+                             hipStream_t stream, int num_cu);
 
 // Copies the host twiddle table to the current device; returns its device address.
 hipError_t upload_twiddles(const void* host, size_t bytes, const float2** dev_ptr);

@@ -64,14 +64,23 @@ constexpr bool plan_is_consistent(int logn) {
   return prod == (1 << logn);
 }
 
-// Twiddles of pass q >= 1: W_{Ns*R}^{r*k}, k < Ns, 1 <= r < R, stored at [(r-1)*Ns + k].
+// Twiddles of pass q >= 1 with radix R: butterfly k < Ns multiplies its input r by
+// W_{Ns*R}^{r*k}, 1 <= r < R.  Only the first tw_loaded(R) powers are stored, at
+// [k*L + r - 1] for 1 <= r <= L (L = tw_loaded(R), even, so a butterfly reads them as
+// 16-byte pairs); the kernels form the others as products, W^{rk} = W^{(r-L)k} W^{Lk}.
+// Every table read costs a vector-memory instruction, and those, not the arithmetic,
+// bound the row kernels when each power is read on its own.
+constexpr int tw_loaded(int R) { return R >= 8 ? 4 : 2; }
 constexpr int pass_table_size(int logn, int q) {
-  return q == 0 ? 0 : (radix(logn, q) - 1) * stride_before(logn, q);
+  return q == 0 ? 0 : tw_loaded(radix(logn, q)) * stride_before(logn, q);
 }
 
 // Post-pass twiddles, 0 <= k < N/2, with the post-pass scale folded in (exact: powers of two):
 //   forward  [k]       = (1/2) * (-i) * W_n^k
 //   inverse  [N/2 + k] = (1/n) * i * conj(W_n^k),   W_n^k = exp(-2 pi i k / (2N)).
+// A thread reads the entry of its first bin only: its other bins lie N/R apart (R the
+// radix of the last pass, or of the first for the inverse), and W_n^{N/R} = W_{2R} is a
+// compile-time constant.
 constexpr int post_table_size(int logn) { return 2 * ((1 << logn) / 2); }
 
 constexpr int plan_table_size(int logn) {

@@ -11,7 +11,7 @@
 namespace rdfft {
 
 // The library's only device-resident data: the twiddle factors of every plan.
-__device__ float2 g_twiddles[kTableEntries];
+__device__ __attribute__((aligned(16))) float2 g_twiddles[kTableEntries];
 
 template <int LOGN, class Acc, class Elem, bool INV>
 __global__ void __launch_bounds__(RowPlan<LOGN>::WG) rdfft_rows_kernel(Elem* buf, int64_t rows,
@@ -31,7 +31,7 @@ __global__ void __launch_bounds__(RowPlan<LOGN>::WG) rdfft_rows_kernel(Elem* buf
 }
 
 template <int LOGN, class Acc, class Elem, bool INV>
-static hipError_t launch_rows(void* buf, int64_t rows, const float2* tw, hipStream_t stream) {
+static hipError_t launch_rows(void* buf, int64_t rows, const float2* tw, hipStream_t stream, int) {
   using P = RowPlan<LOGN>;
   // keep every launch within the grid limit
   const int64_t max_blocks = (int64_t)1 << 30;
@@ -48,7 +48,7 @@ static hipError_t launch_rows(void* buf, int64_t rows, const float2* tw, hipStre
   return hipSuccess;
 }
 
-using RowLauncher = hipError_t (*)(void*, int64_t, const float2*, hipStream_t);
+using RowLauncher = hipError_t (*)(void*, int64_t, const float2*, hipStream_t, int);
 
 template <int... L>
 static std::array<RowLauncher, sizeof...(L)> make_row_table(bool bf16, bool inv, std::integer_sequence<int, L...>) {
@@ -57,12 +57,12 @@ static std::array<RowLauncher, sizeof...(L)> make_row_table(bool bf16, bool inv,
 }
 
 hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, bool bf16, bool inv, const float2* tw,
-                             hipStream_t stream) {
+                             hipStream_t stream, int num_cu) {
   static const auto seq = std::make_integer_sequence<int, kMaxLogN + 1>{};
   static const std::array<RowLauncher, kMaxLogN + 1> tables[4] = {
       make_row_table(false, false, seq), make_row_table(false, true, seq), make_row_table(true, false, seq),
       make_row_table(true, true, seq)};
-  return tables[(bf16 ? 2 : 0) + (inv ? 1 : 0)][logn](buf, rows, tw, stream);
+  return tables[(bf16 ? 2 : 0) + (inv ? 1 : 0)][logn](buf, rows, tw, stream, num_cu);
 }
 
 hipError_t upload_twiddles(const void* host, size_t bytes, const float2** dev_ptr) {

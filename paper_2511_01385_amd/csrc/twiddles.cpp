@@ -40,8 +40,9 @@ std::vector<HostC32> build_twiddle_table() {
     for (int q = 1; q < num_passes(logn); ++q) {
       const int R = radix(logn, q), Ns = stride_before(logn, q);
       const int off = pass_table_offset(logn, q);
-      for (int r = 1; r < R; ++r)
-        for (int k = 0; k < Ns; ++k) t[(size_t)off + (size_t)(r - 1) * Ns + k] = unit_root((long long)r * k, (long long)Ns * R);
+      const int L = tw_loaded(R);
+      for (int k = 0; k < Ns; ++k)
+        for (int r = 1; r <= L; ++r) t[(size_t)off + (size_t)k * L + r - 1] = unit_root((long long)r * k, (long long)Ns * R);
     }
     const int N = 1 << logn, off = post_table_offset(logn);
     const float inv_n = 1.0f / (2.0f * (float)N);
