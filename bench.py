@@ -9,8 +9,9 @@ One step is one pass of the whole hot path over one batch of synthetic input:
 `value` is the algorithmic bytes of one step (each in-place row read once and
 written once; x, y, gy, dx, the spectra and dc once each) times the steps, over the
 wall time of the timed steps, in GB/s.  Inputs are resident in HBM before timing.
-Every buffer comes from a rotating pool of at least 1 GiB per workload so that no
-step is served from the 256 MB Infinity Cache.
+Every buffer comes from a rotating pool of at least 1 GiB per workload, and step i
+runs the forward on slot i and the inverse on slot i-1, so that no call reads data
+still held in the 256 MB Infinity Cache.
 
 Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
 """
@@ -172,7 +173,6 @@ def main():
                          dc=torch.empty((q, kb, p), dtype=torch.float32, device=dev)))
     torch.cuda.synchronize()
 
-    calls = [(f"rdfft_forward_n{n}", n) for n in NS] + [(f"rdfft_inverse_n{n}", n) for n in NS]
     bytes_of = {f"rdfft_forward_n{n}": 2 * ROWS * n * 2 for n in NS}
     bytes_of.update({f"rdfft_inverse_n{n}": 2 * ROWS * n * 2 for n in NS})
     bytes_of["bca_forward"] = 2 * T * d * 2 + q * kb * p * 2
@@ -183,10 +183,19 @@ def main():
         order += [f"rdfft_forward_n{n}", f"rdfft_inverse_n{n}"]
     order += ["bca_forward", "bca_backward"]
 
+    # Step i transforms pool slot i forward and slot i-1 (made spectral by step i-1)
+    # back, so every inverse reads a buffer that was written more than a step's worth
+    # of traffic (> 4 GB) earlier, never the forward output still held in the 256 MB
+    # Infinity Cache.  Each slot returns to its input after its inverse.
+    for n in NS:
+        api.rdfft_forward(pools[n][-1])
+
     def run_step(i, events=None):
         for n in NS:
-            buf = pools[n][i % len(pools[n])]
-            for name, fn in ((f"rdfft_forward_n{n}", api.rdfft_forward), (f"rdfft_inverse_n{n}", api.rdfft_inverse)):
+            pool = pools[n]
+            calls = ((f"rdfft_forward_n{n}", api.rdfft_forward, pool[i % len(pool)]),
+                     (f"rdfft_inverse_n{n}", api.rdfft_inverse, pool[(i - 1) % len(pool)]))
+            for name, fn, buf in calls:
                 if events is not None:
                     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     e0.record(stream)
@@ -195,7 +204,8 @@ def main():
                     events[name].append((e0, e1))
                 else:
                     fn(buf)
-        s = sets[i % len(sets)]
+        # the layer backward runs on the previous step's set, whose x is no longer cached
+        s, sb = sets[i % len(sets)], sets[(i - 1) % len(sets)]
         for name in ("bca_forward", "bca_backward"):
             e0 = e1 = None
             if events is not None:
@@ -204,7 +214,7 @@ def main():
             if name == "bca_forward":
                 api.bca_forward(s["x"], s["c"], s["y"])
             else:
-                api.bca_backward(s["x"], s["c"], s["g"], s["dx"], s["dc"])
+                api.bca_backward(sb["x"], sb["c"], sb["g"], sb["dx"], sb["dc"])
             if events is not None:
                 e1.record(stream)
                 events[name].append((e0, e1))

@@ -229,13 +229,157 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
   }
 
   __syncthreads();
-  // fold this workgroup's partial sums into dc; workgroups start at different offsets
-  // so that they do not all contend for the same addresses at once
-  const int shift = (int)(((unsigned)blockIdx.x * 2654435761u) % (unsigned)((qkn + WG - 1) / WG)) * WG;
+  // fold this workgroup's partial sums into dc; workgroup b starts 64*b slots in, so
+  // that the workgroups, which all finish together, do not queue on the same addresses
+  const int shift = (int)(((unsigned)blockIdx.x * 64u) % (unsigned)qkn);
   for (int e0 = tid; e0 < qkn; e0 += WG) {
     int e = e0 + shift;
     if (e >= qkn) e -= qkn;
     const float2 v = acc[e];
+    unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
+    unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
+  }
+}
+
+// Backward for square layers (q == kb == QB) with few blocks: every thread owns a fixed
+// set of (bin, input block) slots for the whole kernel, keeps C_ij[k] and its dC_ij[k]
+// partial sums for them in registers, and so touches LDS only to read X_j[k], G_i[k]
+// and to write dX_j[k].  With TB > 1 threads per bin (WG > N), the TB threads of a bin
+// split the input blocks j into TJ groups and the tokens of a tile into TS phases; with
+// BT > 1 bins per thread (N > WG) a thread takes bins kt, kt+WG, ...
+constexpr int gcd_int(int a, int b) { return b == 0 ? a : gcd_int(b, a % b); }
+
+template <int LOGN, int QB, int WG>
+struct BcaSq {
+  static constexpr int N = BcaPlan<LOGN>::N;
+  static constexpr int TB = WG >= N ? WG / N : 1;
+  static constexpr int BT = WG >= N ? 1 : N / WG;
+  static constexpr int TJ = gcd_int(TB, QB);  // input-block groups per bin
+  static constexpr int TS = TB / TJ;          // token phases per bin
+  static constexpr int JPT = QB / TJ;         // input blocks per thread
+  static constexpr int NSL = QB * JPT;        // (i, j) slots per bin per thread
+};
+
+template <int LOGN, class Elem, int QB, int WG = BcaPlan<LOGN>::BWD_WG>
+__global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
+                                                                      const Elem* gy, Elem* dx, float* __restrict__ dc,
+                                                                      int64_t tokens, int tt_per_tile, int64_t ntiles,
+                                                                      const float2* __restrict__ tw) {
+  using B = BcaPlan<LOGN>;
+  using S = BcaSq<LOGN, QB, WG>;
+  using In = typename Acc<Elem>::In;
+  using Out = typename Acc<Elem>::Out;
+  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
+  constexpr int TB = S::TB, BT = S::BT, TJ = S::TJ, TS = S::TS, JPT = S::JPT, NSL = S::NSL;
+  const int tid = threadIdx.x;
+  const int grp = tid / TPR, t = tid - grp * TPR;
+  const int u = TB > 1 ? tid / N : 0;         // which of the bin's TB threads
+  const int kt = TB > 1 ? tid - u * N : tid;  // first bin of this thread
+  const int j0 = (u % TJ) * JPT;              // first input block of this thread
+  const int tu = u / TJ;                      // token phase
+  const int TT = tt_per_tile;
+  float2* const xs = bca_lds;                         // TT*QB regions: X, then dX
+  float2* const gs = bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: G
+  float2* const dummy = bca_lds + (size_t)TT * 2 * QB * REG;
+
+  // slot (i, jj) is sl = i*JPT + jj, for input block j = j0 + jj.  C is kept in its
+  // storage form (half the registers for bf16) and widened where it is used.
+  typename In::raw_t cr[BT][NSL];
+  float2 dcr[BT][NSL];
+  {
+    const In cin{c};
+    static_for<BT>([&](auto wc) {
+      constexpr int w = decltype(wc)::value;
+      static_for<NSL>([&](auto sc) {
+        constexpr int sl = decltype(sc)::value, i = sl / JPT, jj = sl % JPT;
+        cr[w][sl] = cin.load_raw((i * QB + j0 + jj) * N + kt + w * WG);  // C_ij[k]
+        dcr[w][sl] = make_float2(0.f, 0.f);
+      });
+    });
+  }
+
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t tok0 = tile * TT;
+    const int nvalid = (int)(tokens - tok0 < TT ? tokens - tok0 : TT);
+
+    // Phase A: X_j = rdFFT(x_j), G_i = rdFFT(g_i)
+    const int nx = TT * QB, ns = 2 * TT * QB;
+    for (int s0 = 0; s0 < ns; s0 += NG) {
+      const int s = s0 + grp;
+      const bool valid = s < ns;
+      float2* reg = valid ? bca_lds + (size_t)s * REG : dummy;
+      const int sx = s < nx ? s : s - nx;
+      const int tt = sx / QB, j = sx - tt * QB;
+      const bool act = valid && tt < nvalid;
+      const Elem* base = s < nx ? x : gy;
+      const Elem* srcp = base + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N;
+      row_forward<LOGN, true>(t, act, In{srcp}, LdsSpectrum{reg}, reg, tw);
+    }
+    __syncthreads();
+
+    // Phase B: per (token, bin): dC_ij += conj(X_j) . G_i and dX_j = sum_i conj(C_ij) . G_i
+    static_for<BT>([&](auto wc) {
+      constexpr int w = decltype(wc)::value;
+      const int k = kt + w * WG;
+      const int pk = lds_pad(k);
+      auto contract = [&](auto s0c) {
+        constexpr bool S0 = decltype(s0c)::value;
+        for (int tt = tu; tt < nvalid; tt += TS) {
+          float2* xk = xs + ((size_t)tt * QB + j0) * REG + pk;
+          const float2* gk = gs + (size_t)tt * QB * REG + pk;
+          float2 X[JPT], G[QB];
+          static_for<JPT>([&](auto jc) { X[decltype(jc)::value] = xk[decltype(jc)::value * REG]; });
+          static_for<QB>([&](auto ic) { G[decltype(ic)::value] = gk[decltype(ic)::value * REG]; });
+          static_for<JPT>([&](auto jc) {
+            constexpr int jj = decltype(jc)::value;
+            float2 d = make_float2(0.f, 0.f);
+            static_for<QB>([&](auto ic) {
+              constexpr int i = decltype(ic)::value;
+              dcr[w][i * JPT + jj] = slot_mac<S0, true>(dcr[w][i * JPT + jj], X[jj], G[i]);
+              d = slot_mac<S0, true>(d, In::widen(cr[w][i * JPT + jj]), G[i]);
+            });
+            xk[jj * REG] = d;
+          });
+        }
+      };
+      if (k == 0) contract(std::true_type{});
+      else contract(std::false_type{});
+    });
+    __syncthreads();
+
+    // Phase C: dx_j = irdFFT(dX_j)
+    for (int s0 = 0; s0 < nx; s0 += NG) {
+      const int s = s0 + grp;
+      const bool valid = s < nx;
+      const int tt = valid ? s / QB : 0, j = valid ? s - tt * QB : 0;
+      const bool act = valid && tt < nvalid;
+      float2* reg = valid ? xs + (size_t)s * REG : dummy;
+      const Out dst{dx + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N};
+      row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, tw);
+    }
+    __syncthreads();
+  }
+
+  // Fold the partial sums into dc (slot e = (i*QB + j)*N + k, float2).  They are staged
+  // in LDS as [TS][QB*QB*N], the TS token phases summed, and the atomics issued from a
+  // rotated start: workgroup b begins 64*b slots in, so that the workgroups, which all
+  // finish together, do not queue on the same addresses.
+  constexpr int QKN = QB * QB * N;
+  float2* const part = bca_lds;
+  static_for<BT>([&](auto wc) {
+    constexpr int w = decltype(wc)::value;
+    static_for<NSL>([&](auto sc) {
+      constexpr int sl = decltype(sc)::value, i = sl / JPT, jj = sl % JPT;
+      part[(size_t)tu * QKN + (i * QB + j0 + jj) * N + kt + w * WG] = dcr[w][sl];
+    });
+  });
+  __syncthreads();
+  const int shift = (int)(((unsigned)blockIdx.x * 64u) % (unsigned)QKN);
+  for (int e0 = tid; e0 < QKN; e0 += WG) {
+    int e = e0 + shift;
+    if (e >= QKN) e -= QKN;
+    float2 v = part[e];
+    static_for<TS - 1>([&](auto pc) { v = c_add(v, part[(size_t)(decltype(pc)::value + 1) * QKN + e]); });
     unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
     unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
   }
@@ -335,8 +479,49 @@ static hipError_t bwd_impl(const BcaArgs& a, const float2* tw, hipStream_t strea
   return hipGetLastError();
 }
 
+// Square layers with few blocks: register-resident C and dC (bca_backward_sq_kernel)
+constexpr int kSqMaxBlocks = 4;  // q == kb <= 4
+constexpr int kSqMaxSlots = 16;  // C and dC values per thread: bins per thread * q * kb
+
+template <int LOGN, int QB>
+constexpr bool sq_fits() {
+  using S = BcaSq<LOGN, QB, BcaPlan<LOGN>::BWD_WG>;
+  return S::BT * S::NSL <= kSqMaxSlots && S::TS <= 8;  // short rows: many threads per bin
+}
+
+template <int LOGN, class Elem, int QB>
+static hipError_t bwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  constexpr int WG = BcaPlan<LOGN>::BWD_WG;
+  using S = BcaSq<LOGN, QB, WG>;
+  const int TT = tokens_per_tile(LOGN, QB, QB, a.tokens, WG, kLdsLimit);
+  if (TT == 0) return hipErrorInvalidValue;
+  const size_t spectra = (size_t)(TT * 2 * QB + 1) * region_bytes(LOGN);
+  const size_t part = (size_t)S::TS * QB * QB * S::N * sizeof(float2);  // [TS][QB*QB*N]
+  const size_t lds = std::max(spectra, part);
+  if (lds > (size_t)kLdsLimit) return hipErrorInvalidValue;
+  static const hipError_t attr = set_lds_limit(bca_backward_sq_kernel<LOGN, Elem, QB>);
+  if (attr != hipSuccess) return attr;
+  const int64_t tiles = (a.tokens + TT - 1) / TT;
+  const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / WG));
+  const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
+  hipLaunchKernelGGL((bca_backward_sq_kernel<LOGN, Elem, QB>), dim3((unsigned)grid), dim3(WG), lds, stream,
+                     static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<const Elem*>(a.y),
+                     static_cast<Elem*>(a.dx), a.dc, a.tokens, TT, tiles, tw);
+  return hipGetLastError();
+}
+
 using BcaFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t);
 using BcaBwdFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t, int);
+
+template <int LOGN, class Elem, int QB>
+static constexpr BcaBwdFn sq_entry() {
+  if constexpr (sq_fits<LOGN, QB>()) return &bwd_sq_impl<LOGN, Elem, QB>;
+  else return nullptr;
+}
+template <int QB, int... L>
+static std::array<BcaBwdFn, sizeof...(L)> sq_table(bool bf16, std::integer_sequence<int, L...>) {
+  return {(bf16 ? sq_entry<L, uint32_t, QB>() : sq_entry<L, float2, QB>())...};
+}
 
 template <int... L>
 static std::array<BcaFn, sizeof...(L)> fwd_table(bool bf16, std::integer_sequence<int, L...>) {
@@ -370,7 +555,13 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
   hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, a.dc, slots);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.tokens == 0) return e;
-  e = tab[a.bf16 ? 1 : 0][a.logp - 1](a, tw, stream, num_cu);
+  static const std::array<BcaBwdFn, kBcaMaxLogN + 1> sq[2][kSqMaxBlocks] = {
+      {sq_table<1>(false, seq), sq_table<2>(false, seq), sq_table<3>(false, seq), sq_table<4>(false, seq)},
+      {sq_table<1>(true, seq), sq_table<2>(true, seq), sq_table<3>(true, seq), sq_table<4>(true, seq)}};
+  BcaBwdFn fn = nullptr;
+  if (a.q == a.kb && a.q <= kSqMaxBlocks) fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
+  if (fn == nullptr) fn = tab[a.bf16 ? 1 : 0][a.logp - 1];
+  e = fn(a, tw, stream, num_cu);
   if (e != hipSuccess) return e;
   // dc holds sum_t conj(X) . G as packed spectra; transform them in place to time domain
   return launch_rdfft_rows(a.dc, (int64_t)a.q * a.kb, a.logp - 1, false, true, tw, stream, num_cu);
