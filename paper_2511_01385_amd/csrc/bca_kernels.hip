@@ -241,6 +241,118 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
   }
 }
 
+// Forward for square layers (q == kb == QB) with few blocks: a persistent workgroup
+// whose threads own fixed bins for the whole kernel and keep C_ij[k] for them in
+// registers (read from HBM once per workgroup rather than once per token).  With TB > 1
+// threads per bin the TB threads split the output blocks i into TJ groups and the
+// tokens of a tile into TS phases; with BT > 1 bins per thread a thread takes bins kt,
+// kt+WG, ...
+template <int LOGN, int QB, int WG>
+struct BcaSqFwd {
+  static constexpr int N = BcaPlan<LOGN>::N;
+  static constexpr int TB = WG >= N ? WG / N : 1;
+  static constexpr int BT = WG >= N ? 1 : N / WG;
+  static constexpr int TJ = TB % QB == 0 ? QB : (QB % TB == 0 ? TB : 1);  // output-block groups
+  static constexpr int TS = TB / TJ;                                        // token phases
+  static constexpr int IPT = QB / TJ;                                       // output blocks per thread
+  static constexpr int NSL = IPT * QB;
+};
+constexpr int kFwdSqWG = 512;
+
+template <int LOGN, class Elem, int QB, int WG = kFwdSqWG>
+__global__ void __launch_bounds__(WG) bca_forward_sq_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
+                                                                     Elem* y, int64_t tokens, int tt_per_tile,
+                                                                     int64_t ntiles, const float2* __restrict__ tw) {
+  using B = BcaPlan<LOGN>;
+  using S = BcaSqFwd<LOGN, QB, WG>;
+  using In = typename Acc<Elem>::In;
+  using Out = typename Acc<Elem>::Out;
+  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
+  constexpr int TB = S::TB, BT = S::BT, TJ = S::TJ, TS = S::TS, IPT = S::IPT, NSL = S::NSL;
+  static_assert(TJ * IPT == QB && TS * TJ == TB, "inconsistent split");
+  const int tid = threadIdx.x;
+  const int grp = tid / TPR, t = tid - grp * TPR;
+  const int u = TB > 1 ? tid / N : 0;
+  const int kt = TB > 1 ? tid - u * N : tid;
+  const int i0 = (u % TJ) * IPT;  // first output block of this thread
+  const int tu = u / TJ;          // token phase
+  const int TT = tt_per_tile;
+  float2* const xs = bca_lds;                         // TT*QB regions: X
+  float2* const ys = bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: Y
+  float2* const dummy = bca_lds + (size_t)TT * 2 * QB * REG;
+
+  // slot (ii, j) is sl = ii*QB + j for output block i = i0 + ii
+  typename In::raw_t cr[BT][NSL];
+  {
+    const In cin{c};
+    static_for<BT>([&](auto wc) {
+      constexpr int w = decltype(wc)::value;
+      static_for<NSL>([&](auto sc) {
+        constexpr int sl = decltype(sc)::value, ii = sl / QB, j = sl % QB;
+        cr[w][sl] = cin.load_raw(((i0 + ii) * QB + j) * N + kt + w * WG);  // C_ij[k]
+      });
+    });
+  }
+
+  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
+    const int64_t tok0 = tile * TT;
+    const int nvalid = (int)(tokens - tok0 < TT ? tokens - tok0 : TT);
+
+    // Phase A: X_j = rdFFT(x_j)
+    const int nx = TT * QB;
+    for (int s0 = 0; s0 < nx; s0 += NG) {
+      const int s = s0 + grp;
+      const bool valid = s < nx;
+      const int tt = valid ? s / QB : 0, j = valid ? s - tt * QB : 0;
+      const bool act = valid && tt < nvalid;
+      float2* reg = valid ? xs + (size_t)s * REG : dummy;
+      const In src{x + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N};
+      row_forward<LOGN, true>(t, act, src, LdsSpectrum{reg}, reg, tw);
+    }
+    __syncthreads();
+
+    // Phase B: Y_i[k] = sum_j C_ij[k] . X_j[k]
+    static_for<BT>([&](auto wc) {
+      constexpr int w = decltype(wc)::value;
+      const int k = kt + w * WG;
+      const int pk = lds_pad(k);
+      auto block_sum = [&](auto s0c) {
+        constexpr bool S0 = decltype(s0c)::value;
+        for (int tt = tu; tt < nvalid; tt += TS) {
+          const float2* xk = xs + (size_t)tt * QB * REG + pk;
+          float2* yk = ys + ((size_t)tt * QB + i0) * REG + pk;
+          float2 X[QB];
+          static_for<QB>([&](auto jc) { X[decltype(jc)::value] = xk[decltype(jc)::value * REG]; });
+          static_for<IPT>([&](auto ic) {
+            constexpr int ii = decltype(ic)::value;
+            float2 a = make_float2(0.f, 0.f);
+            static_for<QB>([&](auto jc) {
+              constexpr int j = decltype(jc)::value;
+              a = slot_mac<S0, false>(a, In::widen(cr[w][ii * QB + j]), X[j]);
+            });
+            yk[ii * REG] = a;
+          });
+        }
+      };
+      if (k == 0) block_sum(std::true_type{});
+      else block_sum(std::false_type{});
+    });
+    __syncthreads();
+
+    // Phase C: y_i = irdFFT(Y_i)
+    for (int s0 = 0; s0 < nx; s0 += NG) {
+      const int s = s0 + grp;
+      const bool valid = s < nx;
+      const int tt = valid ? s / QB : 0, i = valid ? s - tt * QB : 0;
+      const bool act = valid && tt < nvalid;
+      float2* reg = valid ? ys + (size_t)s * REG : dummy;
+      const Out dst{y + ((act ? tok0 + tt : 0) * QB + i) * (int64_t)N};
+      row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, tw);
+    }
+    __syncthreads();
+  }
+}
+
 // Backward for square layers (q == kb == QB) with few blocks: every thread owns a fixed
 // set of (bin, input block) slots for the whole kernel, keeps C_ij[k] and its dC_ij[k]
 // partial sums for them in registers, and so touches LDS only to read X_j[k], G_i[k]
@@ -484,6 +596,31 @@ constexpr int kSqMaxBlocks = 4;  // q == kb <= 4
 constexpr int kSqMaxSlots = 16;  // C and dC values per thread: bins per thread * q * kb
 
 template <int LOGN, int QB>
+constexpr bool sq_fwd_fits() {
+  using S = BcaSqFwd<LOGN, QB, kFwdSqWG>;
+  return BcaPlan<LOGN>::TPR <= kFwdSqWG / 2 && S::BT * S::NSL <= kSqMaxSlots && S::TS <= 8;
+}
+
+template <int LOGN, class Elem, int QB>
+static hipError_t fwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  constexpr int WG = kFwdSqWG;
+  // two workgroups per CU, or one when a token's spectra need more than half the LDS
+  int TT = tokens_per_tile(LOGN, QB, QB, a.tokens, WG, kLdsLimit / 2);
+  if (TT == 0) TT = tokens_per_tile(LOGN, QB, QB, a.tokens, WG, kLdsLimit);
+  if (TT == 0) return hipErrorInvalidValue;
+  const size_t lds = (size_t)(TT * 2 * QB + 1) * region_bytes(LOGN);
+  static const hipError_t attr = set_lds_limit(bca_forward_sq_kernel<LOGN, Elem, QB>);
+  if (attr != hipSuccess) return attr;
+  const int64_t tiles = (a.tokens + TT - 1) / TT;
+  const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / WG));
+  const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
+  hipLaunchKernelGGL((bca_forward_sq_kernel<LOGN, Elem, QB>), dim3((unsigned)grid), dim3(WG), lds, stream,
+                     static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<Elem*>(a.y), a.tokens,
+                     TT, tiles, tw);
+  return hipGetLastError();
+}
+
+template <int LOGN, int QB>
 constexpr bool sq_fits() {
   using S = BcaSq<LOGN, QB, BcaPlan<LOGN>::BWD_WG>;
   return S::BT * S::NSL <= kSqMaxSlots && S::TS <= 8;  // short rows: many threads per bin
@@ -514,6 +651,16 @@ using BcaFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t);
 using BcaBwdFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t, int);
 
 template <int LOGN, class Elem, int QB>
+static constexpr BcaBwdFn sq_fwd_entry() {
+  if constexpr (sq_fwd_fits<LOGN, QB>()) return &fwd_sq_impl<LOGN, Elem, QB>;
+  else return nullptr;
+}
+template <int QB, int... L>
+static std::array<BcaBwdFn, sizeof...(L)> sq_fwd_table(bool bf16, std::integer_sequence<int, L...>) {
+  return {(bf16 ? sq_fwd_entry<L, uint32_t, QB>() : sq_fwd_entry<L, float2, QB>())...};
+}
+
+template <int LOGN, class Elem, int QB>
 static constexpr BcaBwdFn sq_entry() {
   if constexpr (sq_fits<LOGN, QB>()) return &bwd_sq_impl<LOGN, Elem, QB>;
   else return nullptr;
@@ -541,9 +688,18 @@ bool bca_shape_supported(int logp, int q, int kb, bool backward) {
   return tokens_per_tile(logn, kb, q, 1, 256, kLdsLimit - (int)extra) > 0;
 }
 
-hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream) {
+hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
   static const auto seq = std::make_integer_sequence<int, kBcaMaxLogN + 1>{};
   static const std::array<BcaFn, kBcaMaxLogN + 1> tab[2] = {fwd_table(false, seq), fwd_table(true, seq)};
+  static const std::array<BcaBwdFn, kBcaMaxLogN + 1> sq[2][kSqMaxBlocks] = {
+      {sq_fwd_table<1>(false, seq), sq_fwd_table<2>(false, seq), sq_fwd_table<3>(false, seq),
+       sq_fwd_table<4>(false, seq)},
+      {sq_fwd_table<1>(true, seq), sq_fwd_table<2>(true, seq), sq_fwd_table<3>(true, seq),
+       sq_fwd_table<4>(true, seq)}};
+  if (a.q == a.kb && a.q <= kSqMaxBlocks) {
+    const BcaBwdFn fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
+    if (fn != nullptr) return fn(a, tw, stream, num_cu);
+  }
   return tab[a.bf16 ? 1 : 0][a.logp - 1](a, tw, stream);
 }
 

@@ -161,11 +161,13 @@ int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grad
     return RDFFT_EINVAL;
   }
   const float2* tw = nullptr;
-  st = ensure_device(&tw, nullptr);
+  int num_cu = 0;
+  st = ensure_device(&tw, &num_cu);
   if (st != RDFFT_OK) return st;
   rdfft::BcaArgs a{x, c_spectra, y, nullptr, nullptr, tokens, sh.q, sh.kb, sh.logp, dtype == RDFFT_BF16};
-  return rdfft::launch_bca_forward(a, tw, reinterpret_cast<hipStream_t>(stream)) == hipSuccess ? RDFFT_OK
-                                                                                               : RDFFT_ELAUNCH;
+  return rdfft::launch_bca_forward(a, tw, reinterpret_cast<hipStream_t>(stream), num_cu) == hipSuccess
+             ? RDFFT_OK
+             : RDFFT_ELAUNCH;
 }
 
 int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* grads, int64_t d_in, int64_t d_out,

@@ -29,7 +29,7 @@ struct BcaArgs {
   bool bf16;
 };
 
-hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream);
+hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu);
 // also zeroes dc first and transforms it to the time domain afterwards
 hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu);
 
