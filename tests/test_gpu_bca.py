@@ -39,6 +39,16 @@ SMALL = [
     (5, 2048, 2048, 2048, "bf16"),
     (3, 4096, 4096, 4096, "f32"),
     (3, 8192, 8192, 8192, "f32"),
+    # square layers (q == kb) across the register-resident kernels' thread splits, and
+    # square shapes that fall back to the general kernels (too many slots, or q > 4)
+    (13, 32, 32, 16, "bf16"),
+    (21, 96, 96, 32, "f32"),
+    (17, 512, 512, 128, "bf16"),
+    (10, 1536, 1536, 512, "f32"),
+    (7, 4096, 4096, 2048, "bf16"),
+    (5, 8192, 8192, 4096, "f32"),
+    (4, 6144, 6144, 2048, "bf16"),
+    (9, 256, 256, 16, "f32"),
 ]
 
 
