@@ -86,6 +86,21 @@ RDFFT_API int rdfft_forward(void *buf, int64_t rows, int64_t n, int dtype, rdfft
  */
 RDFFT_API int rdfft_inverse(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);
 
+/*
+ * rdfft_pairs_to_halfcomplex / rdfft_halfcomplex_to_pairs -- in-place change of
+ * the packed layout of `rows` spectra between the pairs layout above and the
+ * paper's halfcomplex layout (Sec. 4.1, "Memory Layout"):
+ *   halfcomplex: slot k = Re Y_k for 0 <= k <= n/2, slot n-k = Im Y_k for
+ *                1 <= k < n/2
+ * (so pair slot k, i.e. elements 2k and 2k+1, maps to elements k and n-k, and
+ * pair slot 0 to elements 0 and n/2).  Values are moved bit for bit; NaN
+ * payloads included.  rdfft_inverse expects the pairs layout, so a spectrum
+ * converted to halfcomplex must be converted back before it is inverted.
+ * Arguments and errors as rdfft_forward.
+ */
+RDFFT_API int rdfft_pairs_to_halfcomplex(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);
+RDFFT_API int rdfft_halfcomplex_to_pairs(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);
+
 /* Gradient outputs of bca_backward. */
 typedef struct {
   void *dx;  /* [tokens][d_in] in dtype: dL/dx */

@@ -24,6 +24,8 @@ RDFFT_EDEVICE = -4
 EXPORTS = (
     "rdfft_forward",
     "rdfft_inverse",
+    "rdfft_pairs_to_halfcomplex",
+    "rdfft_halfcomplex_to_pairs",
     "bca_forward",
     "bca_backward",
     "rdfft_init",
@@ -49,7 +51,7 @@ def load() -> ctypes.CDLL:
         raise ImportError(f"{LIB_PATH} is not built; run paper_2511_01385_amd.build.build() first")
     lib = ctypes.CDLL(LIB_PATH)
     vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
-    for name in ("rdfft_forward", "rdfft_inverse"):
+    for name in ("rdfft_forward", "rdfft_inverse", "rdfft_pairs_to_halfcomplex", "rdfft_halfcomplex_to_pairs"):
         f = getattr(lib, name)
         f.argtypes = [vp, i64, i64, i32, vp]
         f.restype = i32

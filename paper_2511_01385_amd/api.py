@@ -61,6 +61,24 @@ def rdfft_inverse(buf: torch.Tensor) -> torch.Tensor:
     return buf
 
 
+def rdfft_pairs_to_halfcomplex(buf: torch.Tensor) -> torch.Tensor:
+    """In place: each packed spectrum row moves from the pairs to the halfcomplex layout."""
+    n = buf.shape[-1]
+    rows = buf.numel() // n if n else 0
+    st = _lib.load().rdfft_pairs_to_halfcomplex(_dev(buf, "buf"), rows, n, _code(buf), _stream(buf))
+    _check(st, "rdfft_pairs_to_halfcomplex")
+    return buf
+
+
+def rdfft_halfcomplex_to_pairs(buf: torch.Tensor) -> torch.Tensor:
+    """In place: each packed spectrum row moves from the halfcomplex to the pairs layout."""
+    n = buf.shape[-1]
+    rows = buf.numel() // n if n else 0
+    st = _lib.load().rdfft_halfcomplex_to_pairs(_dev(buf, "buf"), rows, n, _code(buf), _stream(buf))
+    _check(st, "rdfft_halfcomplex_to_pairs")
+    return buf
+
+
 def bca_forward(x: torch.Tensor, c_spectra: torch.Tensor, y: torch.Tensor) -> torch.Tensor:
     """y[t] = W x[t] for the block-circulant W whose packed block spectra are ``c_spectra`` (q, kb, p)."""
     q, kb, p = c_spectra.shape

@@ -103,6 +103,18 @@ int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stre
   return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
 }
 
+int convert(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream, bool to_hc) {
+  int st = check_transform(buf, rows, n, dtype);
+  if (st != RDFFT_OK || rows == 0) return st;
+  // the kernels need no twiddles, but the device check is the same
+  const float2* tw = nullptr;
+  st = ensure_device(&tw, nullptr);
+  if (st != RDFFT_OK) return st;
+  const hipError_t e = rdfft::launch_layout_convert(buf, rows, ilog2(n) - 1, dtype == RDFFT_BF16, to_hc,
+                                                    reinterpret_cast<hipStream_t>(stream));
+  return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
+}
+
 struct BcaShape {
   int q = 0, kb = 0, logp = 0;
   int64_t x_bytes = 0, y_bytes = 0, c_bytes = 0, dc_bytes = 0;
@@ -145,6 +157,14 @@ int rdfft_forward(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t 
 
 int rdfft_inverse(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
   return transform(buf, rows, n, dtype, stream, true);
+}
+
+int rdfft_pairs_to_halfcomplex(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+  return convert(buf, rows, n, dtype, stream, true);
+}
+
+int rdfft_halfcomplex_to_pairs(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+  return convert(buf, rows, n, dtype, stream, false);
 }
 
 int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grads, int64_t d_in, int64_t d_out,

@@ -15,6 +15,11 @@ namespace rdfft {
 hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, bool bf16, bool inv, const float2* tw,
                              hipStream_t stream, int num_cu);
 
+// In-place conversion of `rows` packed spectra of 2^(logn+1) elements between the pairs
+// layout and the halfcomplex layout (rows >= 1).
+hipError_t launch_layout_convert(void* buf, int64_t rows, int logn, bool bf16, bool to_halfcomplex,
+                                 hipStream_t stream);
+
 // Copies the host twiddle table to the current device; returns its device address.
 hipError_t upload_twiddles(const void* host, size_t bytes, const float2** dev_ptr);
 

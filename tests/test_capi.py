@@ -81,7 +81,7 @@ def test_status_strings(lib):
     ],
 )
 def test_transform_validation(lib, args, want):
-    for fn in (lib.rdfft_forward, lib.rdfft_inverse):
+    for fn in (lib.rdfft_forward, lib.rdfft_inverse, lib.rdfft_pairs_to_halfcomplex, lib.rdfft_halfcomplex_to_pairs):
         assert fn(args[0], args[1], args[2], args[3], None) == want
 
 
@@ -89,6 +89,8 @@ def test_zero_rows_is_a_no_op(lib):
     # returns before any HIP call, so a null buffer is fine
     assert lib.rdfft_forward(None, 0, 64, F32, None) == OK
     assert lib.rdfft_inverse(None, 0, 4096, BF16, None) == OK
+    assert lib.rdfft_pairs_to_halfcomplex(None, 0, 64, BF16, None) == OK
+    assert lib.rdfft_halfcomplex_to_pairs(None, 0, 65536, F32, None) == OK
 
 
 def _grads(dx, dc):
