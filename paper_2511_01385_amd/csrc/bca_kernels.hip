@@ -125,12 +125,19 @@ __global__ void __launch_bounds__(WG) bca_forward_kernel(const Elem* __restrict_
   }
 }
 
-// gy: [T][q*N] pairs (read), dx: [T][kb*N] pairs (written; may alias gy when kb == q),
-// dc: [q][kb][N] float2 slots, receives the spectral partial sums (atomically)
+// General backward.  gy: [T][q*N] pairs (read), dx: [T][kb*N] pairs (written; may alias
+// gy when kb == q), dc: [q][kb][N] float2 slots, receives spectral partial sums (atomically).
+// A launch covers the output blocks i0 <= i < i0+ia and input blocks j0 <= j < j0+jb and
+// does the dx path (mode & kBwdDx; needs every block: i0 = j0 = 0, ia = q, jb = kb), the dC
+// accumulation (mode & kBwdDc), or both.  Layers whose q*kb*(p/2) dC slots do not fit
+// in LDS run one dx launch and then dC launches over block ranges that do.
+constexpr int kBwdDx = 1, kBwdDc = 2;
+
 template <int LOGN, class Elem, int WG = BcaPlan<LOGN>::BWD_WG>
 __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
                                                                    const Elem* gy, Elem* dx, float* __restrict__ dc,
-                                                                   int64_t tokens, int q, int kb, int tt_per_tile,
+                                                                   int64_t tokens, int q, int kb, int i0, int ia,
+                                                                   int j0, int jb, int mode, int tt_per_tile,
                                                                    int64_t ntiles, const float2* __restrict__ tw) {
   using B = BcaPlan<LOGN>;
   using In = typename Acc<Elem>::In;
@@ -139,11 +146,12 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
   const int tid = threadIdx.x;
   const int grp = tid / TPR, t = tid - grp * TPR;
   const int TT = tt_per_tile;
-  float2* const xs = bca_lds;                        // TT*kb regions: X, then dX
-  float2* const gs = bca_lds + (size_t)TT * kb * REG;  // TT*q regions: G
-  float2* const dummy = bca_lds + (size_t)TT * (kb + q) * REG;
-  float2* const acc = dummy + REG;                   // q*kb*N dC partial sums (pair slots)
-  const int qkn = q * kb * N;
+  const bool do_dx = (mode & kBwdDx) != 0, do_dc = (mode & kBwdDc) != 0;
+  float2* const xs = bca_lds;                        // TT*jb regions: X, then dX
+  float2* const gs = bca_lds + (size_t)TT * jb * REG;  // TT*ia regions: G
+  float2* const dummy = bca_lds + (size_t)TT * (jb + ia) * REG;
+  float2* const acc = dummy + REG;                   // ia*jb*N dC partial sums (pair slots)
+  const int qkn = do_dc ? ia * jb * N : 0;
   const In cin{c};
 
   for (int e = tid; e < qkn; e += WG) acc[e] = make_float2(0.f, 0.f);
@@ -152,8 +160,8 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
     const int64_t tok0 = tile * TT;
     const int nvalid = (int)(tokens - tok0 < TT ? tokens - tok0 : TT);
 
-    // Phase A: X_j = rdFFT(x_j), G_i = rdFFT(g_i)
-    const int nx = TT * kb, ns = TT * (kb + q);
+    // Phase A: X_j = rdFFT(x_j), G_i = rdFFT(g_i) for the launch's blocks
+    const int nx = TT * jb, ns = TT * (jb + ia);
     for (int s0 = 0; s0 < ns; s0 += NG) {
       const int s = s0 + grp;
       const bool valid = s < ns;
@@ -163,12 +171,12 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
       const Elem* srcp = x;
       bool act = false;
       if (valid && s < nx) {
-        const int tt = s / kb, j = s - tt * kb;
+        const int tt = s / jb, j = j0 + s - tt * jb;
         act = tt < nvalid;
         srcp = x + ((act ? tok0 + tt : 0) * kb + j) * (int64_t)N;
       } else if (valid) {
         const int sg = s - nx;
-        const int tt = sg / q, i = sg - tt * q;
+        const int tt = sg / ia, i = i0 + sg - tt * ia;
         act = tt < nvalid;
         srcp = gy + ((act ? tok0 + tt : 0) * q + i) * (int64_t)N;
       }
@@ -180,18 +188,22 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
     for (int e = tid; e < qkn; e += WG) {
       const int k = e & (N - 1);
       const int ij = e / N;
-      const int i = ij / kb, j = ij - i * kb;
-      const float2* xp = xs + (size_t)j * REG + lds_pad(k);
-      const float2* gp = gs + (size_t)i * REG + lds_pad(k);
+      const int ii = ij / jb, jj = ij - ii * jb;
+      const float2* xp = xs + (size_t)jj * REG + lds_pad(k);
+      const float2* gp = gs + (size_t)ii * REG + lds_pad(k);
       auto contract = [&](auto s0c) {
         constexpr bool S0 = decltype(s0c)::value;
         float2 sum = acc[e];
 #pragma unroll 4
-        for (int tt = 0; tt < nvalid; ++tt) sum = slot_mac<S0, true>(sum, xp[(size_t)tt * kb * REG], gp[(size_t)tt * q * REG]);
+        for (int tt = 0; tt < nvalid; ++tt) sum = slot_mac<S0, true>(sum, xp[(size_t)tt * jb * REG], gp[(size_t)tt * ia * REG]);
         acc[e] = sum;
       };
       if (k == 0) contract(std::true_type{});
       else contract(std::false_type{});
+    }
+    if (!do_dx) {
+      __syncthreads();
+      continue;
     }
     __syncthreads();
 
@@ -228,6 +240,7 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
     __syncthreads();
   }
 
+  if (!do_dc) return;
   __syncthreads();
   // fold this workgroup's partial sums into dc; workgroup b starts 64*b slots in, so
   // that the workgroups, which all finish together, do not queue on the same addresses
@@ -236,8 +249,12 @@ __global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict
     int e = e0 + shift;
     if (e >= qkn) e -= qkn;
     const float2 v = acc[e];
-    unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
-    unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
+    const int k = e & (N - 1);
+    const int ij = e / N;
+    const int ii = ij / jb, jj = ij - ii * jb;
+    const int64_t d = ((int64_t)(i0 + ii) * kb + (j0 + jj)) * N + k;
+    unsafeAtomicAdd(dc + 2 * d, v.x);
+    unsafeAtomicAdd(dc + 2 * d + 1, v.y);
   }
 }
 
@@ -573,12 +590,13 @@ static hipError_t fwd_impl(const BcaArgs& a, const float2* tw, hipStream_t strea
 static int64_t dc_lds_bytes(int logn, int q, int kb) { return (int64_t)q * kb * ((int64_t)1 << logn) * 8; }
 
 template <int LOGN, class Elem>
-static hipError_t bwd_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+static hipError_t bwd_launch(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu, int i0, int ia,
+                             int j0, int jb, int mode) {
   constexpr int WG = BcaPlan<LOGN>::BWD_WG;
-  const int64_t acc_bytes = dc_lds_bytes(LOGN, a.q, a.kb);
-  const int TT = tokens_per_tile(LOGN, a.kb, a.q, a.tokens, WG, kLdsLimit - (int)acc_bytes);
+  const int64_t acc_bytes = (mode & kBwdDc) ? dc_lds_bytes(LOGN, ia, jb) : 0;
+  const int TT = tokens_per_tile(LOGN, jb, ia, a.tokens, WG, kLdsLimit - (int)acc_bytes);
   if (TT == 0) return hipErrorInvalidValue;
-  const size_t lds = (size_t)(TT * (a.kb + a.q) + 1) * region_bytes(LOGN) + (size_t)acc_bytes;
+  const size_t lds = (size_t)(TT * (jb + ia) + 1) * region_bytes(LOGN) + (size_t)acc_bytes;
   static const hipError_t attr = set_lds_limit(bca_backward_kernel<LOGN, Elem>);
   if (attr != hipSuccess) return attr;
   const int64_t tiles = (a.tokens + TT - 1) / TT;
@@ -587,8 +605,45 @@ static hipError_t bwd_impl(const BcaArgs& a, const float2* tw, hipStream_t strea
   const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
   hipLaunchKernelGGL((bca_backward_kernel<LOGN, Elem>), dim3((unsigned)grid), dim3(WG), lds, stream,
                      static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<const Elem*>(a.y),
-                     static_cast<Elem*>(a.dx), a.dc, a.tokens, a.q, a.kb, TT, tiles, tw);
+                     static_cast<Elem*>(a.dx), a.dc, a.tokens, a.q, a.kb, i0, ia, j0, jb, mode, TT, tiles, tw);
   return hipGetLastError();
+}
+
+// Largest block ranges (ia output x jb input blocks) whose dC slots and spectra fit in LDS
+// together with one token (0 when even one block does not fit).
+static void dc_chunk(int logn, int q, int kb, int* ia, int* jb) {
+  const int64_t rb = region_bytes(logn), blk = dc_lds_bytes(logn, 1, 1);
+  int best_a = 0, best_b = 0;
+  for (int A = 1; A <= q; ++A) {
+    for (int Bj = kb; Bj >= 1; --Bj) {
+      if (A * Bj * blk + (int64_t)(A + Bj + 1) * rb <= kLdsLimit) {
+        const int64_t chunks = (int64_t)((q + A - 1) / A) * ((kb + Bj - 1) / Bj);
+        const int64_t best = best_a ? (int64_t)((q + best_a - 1) / best_a) * ((kb + best_b - 1) / best_b) : INT64_MAX;
+        if (chunks < best) best_a = A, best_b = Bj;
+        break;
+      }
+    }
+  }
+  *ia = best_a;
+  *jb = best_b;
+}
+
+template <int LOGN, class Elem>
+static hipError_t bwd_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  constexpr int WG = BcaPlan<LOGN>::BWD_WG;
+  const int64_t acc_bytes = dc_lds_bytes(LOGN, a.q, a.kb);
+  if (acc_bytes < kLdsLimit && tokens_per_tile(LOGN, a.kb, a.q, a.tokens, WG, kLdsLimit - (int)acc_bytes) > 0)
+    return bwd_launch<LOGN, Elem>(a, tw, stream, num_cu, 0, a.q, 0, a.kb, kBwdDx | kBwdDc);
+  // too many blocks for one LDS-resident dC: the dx path, then dC over block ranges
+  hipError_t e = bwd_launch<LOGN, Elem>(a, tw, stream, num_cu, 0, a.q, 0, a.kb, kBwdDx);
+  int ia = 0, jb = 0;
+  dc_chunk(LOGN, a.q, a.kb, &ia, &jb);
+  if (ia == 0) return hipErrorInvalidValue;
+  for (int i0 = 0; i0 < a.q && e == hipSuccess; i0 += ia)
+    for (int j0 = 0; j0 < a.kb && e == hipSuccess; j0 += jb)
+      e = bwd_launch<LOGN, Elem>(a, tw, stream, num_cu, i0, std::min(ia, a.q - i0), j0, std::min(jb, a.kb - j0),
+                                 kBwdDc);
+  return e;
 }
 
 // Square layers with few blocks: register-resident C and dC (bca_backward_sq_kernel)
@@ -682,10 +737,13 @@ static std::array<BcaBwdFn, sizeof...(L)> bwd_table(bool bf16, std::integer_sequ
 bool bca_shape_supported(int logp, int q, int kb, bool backward) {
   const int logn = logp - 1;
   if (logn < 0 || logn > kBcaMaxLogN) return false;
-  // the backward keeps q*kb*p/2 dC pair slots in LDS next to one token's spectra
-  const int64_t extra = backward ? dc_lds_bytes(logn, q, kb) : 0;
-  if (extra >= kLdsLimit) return false;
-  return tokens_per_tile(logn, kb, q, 1, 256, kLdsLimit - (int)extra) > 0;
+  // one token's spectra must fit in LDS; the backward also needs room for the dC slots
+  // of at least one block next to two spectra (block ranges cover the rest)
+  if (tokens_per_tile(logn, kb, q, 1, 256, kLdsLimit) == 0) return false;
+  if (!backward) return true;
+  int ia = 0, jb = 0;
+  dc_chunk(logn, q, kb, &ia, &jb);
+  return ia > 0;
 }
 
 hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {

@@ -49,6 +49,10 @@ SMALL = [
     (5, 8192, 8192, 4096, "f32"),
     (4, 6144, 6144, 2048, "bf16"),
     (9, 256, 256, 16, "f32"),
+    # layers whose dC slots exceed LDS: one dx launch, then dC over block ranges
+    (5, 4096, 4096, 128, "bf16"),
+    (3, 2048, 4096, 64, "f32"),
+    (7, 4096, 2048, 256, "f32"),
 ]
 
 
