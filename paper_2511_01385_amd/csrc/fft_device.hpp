@@ -239,19 +239,19 @@ __device__ __forceinline__ void row_sync() {
 }
 
 // ----------------------------------------------------------------------------------
-template <int LOGN>
+template <int LOGN, int CH = kChunks[LOGN]>
 struct RowPlan {
   static constexpr int N = 1 << LOGN;
   static constexpr int NP = num_passes(LOGN);
   static constexpr int E = kElems[LOGN];
-  static constexpr int C = kChunks[LOGN];
+  static constexpr int C = CH;
   static constexpr int TPR = N / E;                       // threads per row
   static constexpr int RW = TPR >= 256 ? 1 : 256 / TPR;   // rows per 256-thread workgroup
   static constexpr int WG = TPR * RW;
   // LDS float2 per row: one exchange chunk, or the half-spectrum partner exchange
   static constexpr int LDS_F2 = TPR == 1 ? 0 : lds_padded_size(N / C > N / 2 ? N / C : N / 2);
   static_assert(plan_is_consistent(LOGN), "inconsistent plan");
-  static_assert(C == 1 || E / radix(LOGN, 0) >= C, "chunked exchange needs >= C butterflies per thread");
+
 };
 
 // One Stockham pass q: twiddles (q > 0) then radix-R DFTs on the thread's butterflies.
@@ -290,29 +290,36 @@ __device__ __forceinline__ void stockham_compute(float2* v, int t, const float2*
 
 // Exchange the outputs of pass Q into the inputs of pass Q+1 through LDS.
 // Pass Q writes out[(g/Ns)*Ns*R + (g mod Ns) + r*Ns]; pass Q+1 reads in[g + r*(N/R')].
-// With C chunks, round c moves the outputs whose destination lies in chunk c; for a
-// non-final pass that is decided by the butterfly index b, and for the reads by r.
-template <int LOGN, int Q>
+// With C chunks, round c moves the outputs whose destination lies in chunk c: butterfly
+// g writes into chunk g / (N/(R*C)), which is decided by the butterfly slot b when a
+// thread holds at least C butterflies and by the thread index when it holds one; the
+// reads of round c are those with r in chunk c.
+template <int LOGN, int Q, int CH>
 __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds) {
-  using P = RowPlan<LOGN>;
+  using P = RowPlan<LOGN, CH>;
   constexpr int N = P::N, E = P::E, C = P::C, TPR = P::TPR;
   constexpr int R = radix(LOGN, Q), Ns = stride_before(LOGN, Q), BPT = E / R;
   constexpr int R2 = radix(LOGN, Q + 1), BPT2 = E / R2;
-  constexpr int CH = N / C;
-  static_assert(C == 1 || (BPT % C == 0 && R2 % C == 0), "chunking needs C | BPT and C | R'");
+  constexpr int CS = N / C;  // slots per chunk
+  static_assert(C == 1 || ((BPT % C == 0 || BPT == 1) && R2 % C == 0), "chunking needs C | BPT (or BPT = 1) and C | R'");
   float2 nv[E];
   static_for<C>([&](auto cc) {
     constexpr int c = decltype(cc)::value;
     static_for<BPT>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
-      if constexpr (b / (BPT / C) == c) {
+      auto write = [&]() {
         const int g = t + b * TPR;
         const int k = g & (Ns - 1);
-        const int pb = lds_pad((g - k) * R + k - c * CH);
+        const int pb = lds_pad((g - k) * R + k - c * CS);
         static_for<R>([&](auto rc) {
           constexpr int r = decltype(rc)::value;
           lds[pb + pad_step(r * Ns)] = v[b * R + r];
         });
+      };
+      if constexpr (BPT % C == 0) {
+        if constexpr (b / (BPT / C) == c) write();
+      } else if (t / (TPR / C) == c) {  // one butterfly per thread: no barrier inside
+        write();
       }
     });
     row_sync<TPR>();
@@ -321,7 +328,7 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
       const int pg = lds_pad(t + b * TPR);
       static_for<R2>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
-        // chunk c starts at r = c*R2/C, i.e. at index c*CH: the address is g + (r - c*R2/C)*(N/R2)
+        // chunk c starts at r = c*R2/C, i.e. at index c*CS: the address is g + (r - c*R2/C)*(N/R2)
         if constexpr (r / (R2 / C) == c) nv[b * R2 + r] = lds[pg + pad_step((r - c * (R2 / C)) * (N / R2))];
       });
     });
@@ -330,12 +337,12 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
   static_for<E>([&](auto ic) { v[decltype(ic)::value] = nv[decltype(ic)::value]; });
 }
 
-template <int LOGN, int Q, bool INV>
+template <int LOGN, int Q, bool INV, int CH = kChunks[LOGN]>
 __device__ __forceinline__ void stockham_from(float2* v, int t, float2* lds, const float2* __restrict__ tw) {
   stockham_compute<LOGN, Q, INV>(v, t, tw);
   if constexpr (Q + 1 < RowPlan<LOGN>::NP) {
-    stockham_exchange<LOGN, Q>(v, t, lds);
-    stockham_from<LOGN, Q + 1, INV>(v, t, lds, tw);
+    stockham_exchange<LOGN, Q, CH>(v, t, lds);
+    stockham_from<LOGN, Q + 1, INV, CH>(v, t, lds, tw);
   }
 }
 
@@ -369,7 +376,7 @@ __device__ __forceinline__ void load_forward(int t, const Src& src, typename Src
   }
 }
 
-template <int LOGN, bool DST_IN_LDS, class Src, class Dst>
+template <int LOGN, bool DST_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN]>
 __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typename Src::raw_t* raw,
                                                    const Dst& dst, float2* lds, const float2* __restrict__ tw) {
   using P = RowPlan<LOGN>;
@@ -383,7 +390,7 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
   } else {
     float2 v[E];
     static_for<E>([&](auto ic) { v[decltype(ic)::value] = Src::widen(raw[decltype(ic)::value]); });
-    stockham_from<LOGN, 0, false>(v, t, lds, tw);
+    stockham_from<LOGN, 0, false, CH>(v, t, lds, tw);
 
     // Post-pass.  After the last pass thread t holds Z_m at m = g_b + r*(N/RL).
     constexpr int RL = radix(LOGN, P::NP - 1), BPL = E / RL, NsL = N / RL;
@@ -466,12 +473,12 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
   }
 }
 
-template <int LOGN, bool DST_IN_LDS, class Src, class Dst>
+template <int LOGN, bool DST_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN]>
 __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, const Dst& dst, float2* lds,
                                             const float2* __restrict__ tw) {
   typename Src::raw_t raw[RowPlan<LOGN>::E];
   load_forward<LOGN>(t, src, raw);
-  row_forward_loaded<LOGN, DST_IN_LDS, Src>(t, active, raw, dst, lds, tw);
+  row_forward_loaded<LOGN, DST_IN_LDS, Src, Dst, CH>(t, active, raw, dst, lds, tw);
 }
 
 // ----------------------------------------------------------------------------------
@@ -505,7 +512,7 @@ __device__ __forceinline__ void load_inverse(int t, const Src& src, typename Src
   }
 }
 
-template <int LOGN, bool SRC_IN_LDS, class Src, class Dst>
+template <int LOGN, bool SRC_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN]>
 __device__ __forceinline__ void row_inverse_loaded(int t, bool active, const typename Src::raw_t* raw,
                                                    const Dst& dst, float2* lds, const float2* __restrict__ tw) {
   using P = RowPlan<LOGN>;
@@ -592,7 +599,7 @@ __device__ __forceinline__ void row_inverse_loaded(int t, bool active, const typ
       });
       row_sync<TPR>();
     }
-    stockham_from<LOGN, 0, true>(v, t, lds, tw);
+    stockham_from<LOGN, 0, true, CH>(v, t, lds, tw);
     if (!active) return;
     constexpr int RL = radix(LOGN, P::NP - 1), BPL = E / RL, NsL = N / RL;
     static_for<BPL>([&](auto bc) {
@@ -606,12 +613,12 @@ __device__ __forceinline__ void row_inverse_loaded(int t, bool active, const typ
   }
 }
 
-template <int LOGN, bool SRC_IN_LDS, class Src, class Dst>
+template <int LOGN, bool SRC_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN]>
 __device__ __forceinline__ void row_inverse(int t, bool active, const Src& src, const Dst& dst, float2* lds,
                                             const float2* __restrict__ tw) {
   typename Src::raw_t raw[RowPlan<LOGN>::E];
   load_inverse<LOGN>(t, src, raw);
-  row_inverse_loaded<LOGN, SRC_IN_LDS, Src>(t, active, raw, dst, lds, tw);
+  row_inverse_loaded<LOGN, SRC_IN_LDS, Src, Dst, CH>(t, active, raw, dst, lds, tw);
 }
 
 }  // namespace rdfft

@@ -13,10 +13,17 @@ namespace rdfft {
 // The library's only device-resident data: the twiddle factors of every plan.
 __device__ __attribute__((aligned(16))) float2 g_twiddles[kTableEntries];
 
+// exchange rounds per pass of the row kernels
+template <int LOGN, class Acc>
+constexpr int row_chunks() {
+  return std::is_same<Acc, GlobalBF16>::value ? kChunksBf16[LOGN] : kChunks[LOGN];
+}
+
 template <int LOGN, class Acc, class Elem, bool INV>
 __global__ void __launch_bounds__(RowPlan<LOGN>::WG) rdfft_rows_kernel(Elem* buf, int64_t rows,
                                                                         const float2* __restrict__ tw) {
-  using P = RowPlan<LOGN>;
+  constexpr int CH = row_chunks<LOGN, Acc>();
+  using P = RowPlan<LOGN, CH>;
   constexpr int LDS_ROW = P::LDS_F2 > 0 ? P::LDS_F2 : 1;
   __shared__ float2 lds[P::RW * LDS_ROW];
   const int tid = threadIdx.x;
@@ -26,8 +33,8 @@ __global__ void __launch_bounds__(RowPlan<LOGN>::WG) rdfft_rows_kernel(Elem* buf
   const bool active = row < rows;
   const Acc acc{buf + (active ? row : 0) * (int64_t)P::N};
   float2* my = lds + rho * LDS_ROW;
-  if constexpr (!INV) row_forward<LOGN, false>(t, active, acc, acc, my, tw);
-  else row_inverse<LOGN, false>(t, active, acc, acc, my, tw);
+  if constexpr (!INV) row_forward<LOGN, false, Acc, Acc, CH>(t, active, acc, acc, my, tw);
+  else row_inverse<LOGN, false, Acc, Acc, CH>(t, active, acc, acc, my, tw);
 }
 
 template <int LOGN, class Acc, class Elem, bool INV>
