@@ -39,9 +39,9 @@ constexpr int kPlan[kMaxLogN + 1][5] = {
 // pass-to-pass exchange is split into C rounds so that one round fits in LDS.
 constexpr int kElems[kMaxLogN + 1] = {1, 2, 4, 8, 16, 8, 8, 16, 16, 8, 16, 16, 16, 16, 16, 32};
 constexpr int kChunks[kMaxLogN + 1] = {1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 2};
-// The bf16 row kernels of long rows also exchange in two rounds: the halved LDS region
+// The bf16 row kernels of rows n >= 2048 also exchange in two rounds: the halved LDS region
 // admits more resident waves, which pays where the arithmetic, not HBM, bounds the time.
-constexpr int kChunksBf16[kMaxLogN + 1] = {1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 2, 2, 2, 2, 2};
+constexpr int kChunksBf16[kMaxLogN + 1] = {1, 1, 1, 1, 1, 1, 1, 1, 1, 1, 2, 2, 2, 2, 2, 2};
 
 constexpr int num_passes(int logn) {
   int k = 0;
