@@ -294,9 +294,13 @@ __global__ void __launch_bounds__(WG) bca_forward_sq_kernel(const Elem* __restri
   const int i0 = (u % TJ) * IPT;  // first output block of this thread
   const int tu = u / TJ;          // token phase
   const int TT = tt_per_tile;
-  float2* const xs = bca_lds;                         // TT*QB regions: X
-  float2* const ys = bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: Y
-  float2* const dummy = bca_lds + (size_t)TT * 2 * QB * REG;
+  // With one thread per bin, Y_i[k] overwrites X_i[k]: the thread has read every X_j[k]
+  // before it writes, and no other thread touches bin k, so a token needs QB regions.
+  constexpr bool INPLACE = TB == 1;
+  float2* const xs = bca_lds;                                         // TT*QB regions: X
+  float2* const ys = INPLACE ? xs : bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: Y
+  // spare region for row groups without a transform (allocated only when some exist)
+  float2* const dummy = bca_lds + (size_t)TT * (INPLACE ? 1 : 2) * QB * REG;
 
   // slot (ii, j) is sl = ii*QB + j for output block i = i0 + ii
   typename In::raw_t cr[BT][NSL];
@@ -409,6 +413,7 @@ __global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const Elem* __restr
   const int TT = tt_per_tile;
   float2* const xs = bca_lds;                         // TT*QB regions: X, then dX
   float2* const gs = bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: G
+  // spare region for row groups without a transform (allocated only when some exist)
   float2* const dummy = bca_lds + (size_t)TT * 2 * QB * REG;
 
   // slot (i, jj) is sl = i*JPT + jj, for input block j = j0 + jj.  C is kept in its
@@ -650,6 +655,21 @@ static hipError_t bwd_impl(const BcaArgs& a, const float2* tw, hipStream_t strea
 constexpr int kSqMaxBlocks = 4;  // q == kb <= 4
 constexpr int kSqMaxSlots = 16;  // C and dC values per thread: bins per thread * q * kb
 
+// Tokens per tile of the square-layer kernels: the largest TT (at most 64 and the token
+// count) whose TT*rpt spectra, plus a spare region when TT*QB transforms leave some of
+// the ng row groups idle, fit in `budget` bytes.  0 when one token does not fit.
+static int sq_tokens_per_tile(int logn, int rpt, int qb, int ng, int64_t tokens, int64_t budget, bool* spare) {
+  const int64_t rb = region_bytes(logn);
+  for (int tt = (int)std::min<int64_t>(64, std::max<int64_t>(tokens, 1)); tt >= 1; --tt) {
+    const bool sp = (tt * qb) % ng != 0;
+    if ((tt * rpt + (sp ? 1 : 0)) * rb <= budget) {
+      *spare = sp;
+      return tt;
+    }
+  }
+  return 0;
+}
+
 template <int LOGN, int QB>
 constexpr bool sq_fwd_fits() {
   using S = BcaSqFwd<LOGN, QB, kFwdSqWG>;
@@ -659,11 +679,15 @@ constexpr bool sq_fwd_fits() {
 template <int LOGN, class Elem, int QB>
 static hipError_t fwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
   constexpr int WG = kFwdSqWG;
+  using S = BcaSqFwd<LOGN, QB, WG>;
+  constexpr int rpt = (S::TB == 1 ? 1 : 2) * QB;  // regions per token (Y over X when TB == 1)
+  constexpr int ng = WG / BcaPlan<LOGN>::TPR;
   // two workgroups per CU, or one when a token's spectra need more than half the LDS
-  int TT = tokens_per_tile(LOGN, QB, QB, a.tokens, WG, kLdsLimit / 2);
-  if (TT == 0) TT = tokens_per_tile(LOGN, QB, QB, a.tokens, WG, kLdsLimit);
+  bool spare = false;
+  int TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit / 2, &spare);
+  if (TT == 0) TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit, &spare);
   if (TT == 0) return hipErrorInvalidValue;
-  const size_t lds = (size_t)(TT * 2 * QB + 1) * region_bytes(LOGN);
+  const size_t lds = (size_t)(TT * rpt + (spare ? 1 : 0)) * region_bytes(LOGN);
   static const hipError_t attr = set_lds_limit(bca_forward_sq_kernel<LOGN, Elem, QB>);
   if (attr != hipSuccess) return attr;
   const int64_t tiles = (a.tokens + TT - 1) / TT;
@@ -685,9 +709,10 @@ template <int LOGN, class Elem, int QB>
 static hipError_t bwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
   constexpr int WG = BcaPlan<LOGN>::BWD_WG;
   using S = BcaSq<LOGN, QB, WG>;
-  const int TT = tokens_per_tile(LOGN, QB, QB, a.tokens, WG, kLdsLimit);
+  bool spare = false;
+  const int TT = sq_tokens_per_tile(LOGN, 2 * QB, QB, WG / BcaPlan<LOGN>::TPR, a.tokens, kLdsLimit, &spare);
   if (TT == 0) return hipErrorInvalidValue;
-  const size_t spectra = (size_t)(TT * 2 * QB + 1) * region_bytes(LOGN);
+  const size_t spectra = (size_t)(TT * 2 * QB + (spare ? 1 : 0)) * region_bytes(LOGN);
   const size_t part = (size_t)S::TS * QB * QB * S::N * sizeof(float2);  // [TS][QB*QB*N]
   const size_t lds = std::max(spectra, part);
   if (lds > (size_t)kLdsLimit) return hipErrorInvalidValue;
