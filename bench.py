@@ -16,7 +16,9 @@ still held in the 256 MB Infinity Cache.
 roofline: the call with the longest average duration in three untimed probe steps is
 the dominant kernel; inside the timed steps only that call is bracketed by HIP events
 (on its launch stream), and its algorithmic bytes over its average event-timed
-duration give `achieved`.  per_call_probe lists every call from the probe steps.
+duration give `achieved`.  per_call_probe lists every call from the probe steps.  per_config (after the timed steps,
+outside `value`) times every workload shape of the paper's configurations on its own:
+fp32 and bf16 transforms for each n, n = 65536 fp32, and the three layer shapes.
 
 Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
 """
@@ -52,6 +54,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
+    ap.add_argument("--no-configs", action="store_true", help="skip the per-configuration table")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 1 GiB device copy (for HBM counter calibration)")
     return ap.parse_args()
@@ -120,6 +123,82 @@ def cpu_baseline(host_rows, host_bca, min_seconds: float = 10.0):
                   f"{tokens} tokens; bytes counted as the GPU step's bf16 algorithmic bytes; {dt:.1f} s",
         "seconds": round(dt, 2),
     }
+
+
+def config_table(dev, stream, reps: int = 10):
+    """Untimed-by-`value` context: every workload shape of the paper's configurations.
+
+    Batched transforms for each n in 64..4096 (2^16 rows) in fp32 and bf16 storage and
+    n = 65536 (1024 rows, fp32), forward and inverse, each over a rotating >= 1 GiB pool;
+    and the three layer shapes (768-wide p = 256, 4096-wide p = 1024, 8192-wide p = 8192,
+    bf16, 4096 tokens) forward and backward.  GB/s are algorithmic bytes over the
+    event-timed average of `reps` back-to-back calls; frac is of 8 TB/s.
+    """
+    import torch
+
+    from paper_2511_01385_amd import api
+
+    def timed(fn, args_list):
+        for a in args_list[:2]:
+            fn(*a)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for i in range(reps):
+            fn(*args_list[i % len(args_list)])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    table = {}
+    shapes = [(n, ROWS, dt) for dt in ("f32", "bf16") for n in NS] + [(65536, 1024, "f32")]
+    for n, rows, dt in shapes:
+        tdt = torch.float32 if dt == "f32" else torch.bfloat16
+        nb = rows * n * (4 if dt == "f32" else 2)
+        pool = [torch.randn(rows, n, device=dev).to(tdt) for _ in range(max(2, -(-POOL_BYTES // nb)))]
+        # forwards over the whole pool, then inverses in the same order: every buffer
+        # returns to its input and no call finds its data in the Infinity Cache
+        reps_n = len(pool) * ((reps + len(pool) - 1) // len(pool))
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        for b in pool[:1]:
+            api.rdfft_forward(b)
+            api.rdfft_inverse(b)
+        e0.record(stream)
+        for i in range(reps_n):
+            api.rdfft_forward(pool[i % len(pool)])
+        e1.record(stream)
+        for i in range(reps_n):
+            api.rdfft_inverse(pool[i % len(pool)])
+        e2.record(stream)
+        torch.cuda.synchronize()
+        us_f = e0.elapsed_time(e1) * 1e3 / reps_n
+        us_i = e1.elapsed_time(e2) * 1e3 / reps_n
+        gbs_f, gbs_i = 2 * nb / us_f / 1e3, 2 * nb / us_i / 1e3
+        table[f"rdfft_{dt}_n{n}_rows{rows}"] = {
+            "forward_us": round(us_f, 2), "inverse_us": round(us_i, 2),
+            "forward_GB_s": round(gbs_f, 1), "inverse_GB_s": round(gbs_i, 1),
+            "frac": round((gbs_f + gbs_i) / 2 / HBM_PEAK_GBS, 4)}
+        del pool
+    torch.cuda.empty_cache()
+    for d, p in ((768, 256), (4096, 1024), (8192, 8192)):
+        T = 4096
+        q = kb = d // p
+        nset = max(2, -(-POOL_BYTES // (4 * T * d * 2)))
+        sets = [dict(x=torch.randn(T, d, device=dev).to(torch.bfloat16),
+                     c=(0.02 * torch.randn(q, kb, p, device=dev)).to(torch.bfloat16),
+                     g=torch.randn(T, d, device=dev).to(torch.bfloat16),
+                     y=torch.empty(T, d, device=dev, dtype=torch.bfloat16),
+                     dx=torch.empty(T, d, device=dev, dtype=torch.bfloat16),
+                     dc=torch.empty(q, kb, p, device=dev)) for _ in range(nset)]
+        us_f = timed(lambda st: api.bca_forward(st["x"], st["c"], st["y"]), [(st,) for st in sets])
+        us_b = timed(lambda st: api.bca_backward(st["x"], st["c"], st["g"], st["dx"], st["dc"]), [(st,) for st in sets])
+        bf = 2 * T * d * 2 + q * kb * p * 2
+        bb = 3 * T * d * 2 + q * kb * p * 2 + q * kb * p * 4
+        table[f"bca_bf16_d{d}_p{p}_T{T}"] = {
+            "forward_us": round(us_f, 2), "backward_us": round(us_b, 2),
+            "forward_GB_s": round(bf / us_f / 1e3, 1), "backward_GB_s": round(bb / us_b / 1e3, 1)}
+        del sets
+    torch.cuda.empty_cache()
+    return table
 
 
 def copy_rate(dev, stream, reps: int = 5):
@@ -306,6 +385,10 @@ def main():
     copy_gbs = copy_rate(dev, stream)
     out["hbm_copy"] = {"GB_s": copy_gbs, "frac_of_copy": round(value / copy_gbs, 4),
                        "roofline_frac_of_copy": round(dom["GB_s"] / copy_gbs, 4)}
+    if not args.no_configs:
+        del pools, sets
+        torch.cuda.empty_cache()
+        out["per_config"] = config_table(dev, stream)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(host_rows, (x, c, g))
     else:
