@@ -21,8 +21,8 @@
  *   device the first time that device is used (or by rdfft_init()); that first
  *   use performs a synchronous copy and must not happen under stream capture.
  * - dtype selects the storage type of the transformed data; arithmetic is
- *   float32 throughout, bf16 values are widened exactly and rounded to nearest
- *   even on store.
+ *   float32 throughout, bf16 and f16 values are widened exactly and rounded to
+ *   nearest even on store (an f16 result beyond 65504 becomes an infinity).
  *
  * Packed spectrum layout ("pairs"), for a row of even length n:
  *   slot 0 = Y_0 (DC, real), slot 1 = Y_{n/2} (Nyquist, real),
@@ -53,7 +53,8 @@ typedef struct ihipStream_t *rdfft_stream_t;
 
 typedef enum {
   RDFFT_F32 = 0,  /* IEEE float32 storage */
-  RDFFT_BF16 = 1  /* bfloat16 storage */
+  RDFFT_BF16 = 1, /* bfloat16 storage */
+  RDFFT_F16 = 2   /* IEEE float16 storage: transforms and layout converters only */
 } rdfft_dtype_t;
 
 typedef enum {
@@ -121,6 +122,7 @@ typedef struct {
  *              d_in == d_out (a truly in-place layer, Sec. 5.1.1); any other
  *              overlap with x or c_spectra -> RDFFT_EINVAL.
  *   grads      reserved, must be NULL.
+ *   dtype      RDFFT_F32 or RDFFT_BF16 (RDFFT_F16 -> RDFFT_EUNSUPPORTED).
  *   p          power of two, 2 <= p <= 8192 (larger -> RDFFT_EUNSUPPORTED);
  *              must divide d_in and d_out (Table 1 marks such shapes N/A) -> else RDFFT_EINVAL.
  *   tokens     >= 0; 0 is a no-op (x and y may then be NULL).

@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "librdfft.so
 
 RDFFT_F32 = 0
 RDFFT_BF16 = 1
+RDFFT_F16 = 2
 
 RDFFT_OK = 0
 RDFFT_EINVAL = -1

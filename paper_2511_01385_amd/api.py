@@ -25,7 +25,9 @@ def _code(t: torch.Tensor) -> int:
         return _lib.RDFFT_F32
     if t.dtype == torch.bfloat16:
         return _lib.RDFFT_BF16
-    raise TypeError(f"rdfft supports float32 and bfloat16 storage, got {t.dtype}")
+    if t.dtype == torch.float16:
+        return _lib.RDFFT_F16
+    raise TypeError(f"rdfft supports float32, bfloat16 and float16 storage, got {t.dtype}")
 
 
 def _dev(t: torch.Tensor, name: str) -> int:

@@ -803,7 +803,7 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
   e = fn(a, tw, stream, num_cu);
   if (e != hipSuccess) return e;
   // dc holds sum_t conj(X) . G as packed spectra; transform them in place to time domain
-  return launch_rdfft_rows(a.dc, (int64_t)a.q * a.kb, a.logp - 1, false, true, tw, stream, num_cu);
+  return launch_rdfft_rows(a.dc, (int64_t)a.q * a.kb, a.logp - 1, kStorageF32, true, tw, stream, num_cu);
 }
 
 }  // namespace rdfft

@@ -45,7 +45,7 @@ bool overlaps(const void* a, int64_t na, const void* b, int64_t nb) {
   return na > 0 && nb > 0 && x < y + (uintptr_t)nb && y < x + (uintptr_t)na;
 }
 
-int elem_bytes(int dtype) { return dtype == RDFFT_BF16 ? 2 : 4; }
+int elem_bytes(int dtype) { return dtype == RDFFT_F32 ? 4 : 2; }
 
 // products of sizes that must not overflow int64
 bool mul_ok(int64_t a, int64_t b, int64_t* out) {
@@ -80,7 +80,7 @@ int ensure_device(const float2** tw, int* num_cu) {
 }
 
 int check_transform(const void* buf, int64_t rows, int64_t n, int dtype) {
-  if (dtype != RDFFT_F32 && dtype != RDFFT_BF16) return RDFFT_EINVAL;
+  if (dtype != RDFFT_F32 && dtype != RDFFT_BF16 && dtype != RDFFT_F16) return RDFFT_EINVAL;
   if (rows < 0) return RDFFT_EINVAL;
   if (n < 2 || (n & 1)) return RDFFT_EINVAL;
   if (!is_pow2(n) || n > (int64_t(2) << rdfft::kMaxLogN)) return RDFFT_EUNSUPPORTED;
@@ -98,7 +98,7 @@ int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stre
   int num_cu = 0;
   st = ensure_device(&tw, &num_cu);
   if (st != RDFFT_OK) return st;
-  const hipError_t e = rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype == RDFFT_BF16, inv, tw,
+  const hipError_t e = rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype, inv, tw,
                                                 reinterpret_cast<hipStream_t>(stream), num_cu);
   return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
 }
@@ -110,7 +110,7 @@ int convert(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream
   const float2* tw = nullptr;
   st = ensure_device(&tw, nullptr);
   if (st != RDFFT_OK) return st;
-  const hipError_t e = rdfft::launch_layout_convert(buf, rows, ilog2(n) - 1, dtype == RDFFT_BF16, to_hc,
+  const hipError_t e = rdfft::launch_layout_convert(buf, rows, ilog2(n) - 1, dtype != RDFFT_F32, to_hc,
                                                     reinterpret_cast<hipStream_t>(stream));
   return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
 }
@@ -122,6 +122,7 @@ struct BcaShape {
 
 int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t d_out, int64_t p, int64_t tokens,
               int dtype, bool backward, BcaShape* sh) {
+  if (dtype == RDFFT_F16) return RDFFT_EUNSUPPORTED;  // the layer kernels store f32 or bf16
   if (dtype != RDFFT_F32 && dtype != RDFFT_BF16) return RDFFT_EINVAL;
   if (tokens < 0 || d_in <= 0 || d_out <= 0 || p <= 0) return RDFFT_EINVAL;
   if (p < 2 || (p & 1)) return RDFFT_EINVAL;

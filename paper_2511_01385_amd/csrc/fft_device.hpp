@@ -50,23 +50,31 @@ __device__ __forceinline__ float2 c_mul(float2 a, float2 w) {
   else return make_float2(fmaf(a.x, w.x, a.y * w.y), fmaf(a.y, w.x, -a.x * w.y));
 }
 
-// cos(2 pi m / 32), m in [0, 8]; the rest follows by symmetry
-constexpr double kCos32[9] = {1.0,
-                              0.98078528040323044912618223613424,
-                              0.92387953251128675612818318939679,
-                              0.83146961230254523707878837761791,
-                              0.70710678118654752440084436210485,
-                              0.55557023301960222474283081394853,
-                              0.38268343236508977172845998403040,
-                              0.19509032201612826784828486847702,
-                              0.0};
-constexpr double cos32(int m) {
-  m &= 31;
-  return m <= 8 ? kCos32[m] : m <= 16 ? -kCos32[16 - m] : m <= 24 ? -kCos32[m - 16] : kCos32[32 - m];
+// cos(2 pi m / 64), m in [0, 16]; the rest follows by symmetry
+constexpr double kCos64[17] = {1.0,
+                               0.99518472667219688624483695310948,
+                               0.98078528040323044912618223613424,
+                               0.95694033573220886493579788698027,
+                               0.92387953251128675612818318939679,
+                               0.88192126434835502971275686366039,
+                               0.83146961230254523707878837761791,
+                               0.77301045336273696081090660975847,
+                               0.70710678118654752440084436210485,
+                               0.63439328416364549821517161322549,
+                               0.55557023301960222474283081394853,
+                               0.47139673682599764855638762590867,
+                               0.38268343236508977172845998403040,
+                               0.29028467725446236763619237581740,
+                               0.19509032201612826784828486847702,
+                               0.09801714032956060199419556388864,
+                               0.0};
+constexpr double cos64(int m) {
+  m &= 63;
+  return m <= 16 ? kCos64[m] : m <= 32 ? -kCos64[32 - m] : m <= 48 ? -kCos64[m - 32] : kCos64[64 - m];
 }
-constexpr double sin32(int m) { return cos32(m - 8); }
+constexpr double sin64(int m) { return cos64(m - 16); }
 
-// a * exp(-+ 2 pi i J / R): forward sign unless INV.  R divides 32.
+// a * exp(-+ 2 pi i J / R): forward sign unless INV.  R divides 64.
 template <int R, int J, bool INV>
 __device__ __forceinline__ float2 rot(float2 a) {
   constexpr int j = ((J % R) + R) % R;
@@ -79,9 +87,9 @@ __device__ __forceinline__ float2 rot(float2 a) {
   } else if constexpr (4 * j == 3 * R) {
     return INV ? make_float2(a.y, -a.x) : make_float2(-a.y, a.x);
   } else {
-    static_assert(32 % R == 0, "constant rotations need R | 32");
-    constexpr float c = (float)cos32(j * (32 / R));
-    constexpr float s = (float)sin32(j * (32 / R));
+    static_assert(64 % R == 0, "constant rotations need R | 64");
+    constexpr float c = (float)cos64(j * (64 / R));
+    constexpr float s = (float)sin64(j * (64 / R));
     if constexpr (!INV) return make_float2(fmaf(a.x, c, a.y * s), fmaf(a.y, c, -a.x * s));
     else return make_float2(fmaf(a.x, c, -a.y * s), fmaf(a.y, c, a.x * s));
   }
@@ -188,6 +196,26 @@ struct GlobalBF16 {
   __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return bf16x2_to_f32(base[m]); }
   __device__ __forceinline__ void store(int m, float2 v) const { base[m] = f32_to_bf16x2(v); }
+};
+
+typedef _Float16 f16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ float2 f16x2_to_f32(uint32_t u) {
+  const f32x2_t f = __builtin_convertvector(__builtin_bit_cast(f16x2_t, u), f32x2_t);
+  return make_float2(f.x, f.y);
+}
+__device__ __forceinline__ uint32_t f32_to_f16x2(float2 v) {  // round to nearest even
+  const f32x2_t f = {v.x, v.y};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, f16x2_t));
+}
+
+struct GlobalF16 {
+  using raw_t = uint32_t;
+  uint32_t* base;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return f16x2_to_f32(r); }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
+  __device__ __forceinline__ float2 load(int m) const { return f16x2_to_f32(base[m]); }
+  __device__ __forceinline__ void store(int m, float2 v) const { base[m] = f32_to_f16x2(v); }
 };
 
 // Read-only views (inputs that must never be written)

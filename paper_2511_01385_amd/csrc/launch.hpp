@@ -10,14 +10,17 @@
 
 namespace rdfft {
 
+// Storage types of the row kernels (the values of rdfft_dtype_t)
+constexpr int kStorageF32 = 0, kStorageBF16 = 1, kStorageF16 = 2;
+
 // In-place forward (inv = false) or inverse rdFFT of `rows` rows of 2^(logn+1) elements
-// (rows >= 1); num_cu sizes the persistent grid.
-hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, bool bf16, bool inv, const float2* tw,
+// (rows >= 1) stored as `storage`.
+hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, int storage, bool inv, const float2* tw,
                              hipStream_t stream, int num_cu);
 
 // In-place conversion of `rows` packed spectra of 2^(logn+1) elements between the pairs
-// layout and the halfcomplex layout (rows >= 1).
-hipError_t launch_layout_convert(void* buf, int64_t rows, int logn, bool bf16, bool to_halfcomplex,
+// layout and the halfcomplex layout (rows >= 1); half16 = 16-bit storage (bf16 or f16).
+hipError_t launch_layout_convert(void* buf, int64_t rows, int logn, bool half16, bool to_halfcomplex,
                                  hipStream_t stream);
 
 // Copies the host twiddle table to the current device; returns its device address.

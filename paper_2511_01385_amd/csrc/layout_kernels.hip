@@ -103,13 +103,13 @@ static std::array<LayoutLauncher, sizeof...(L)> make_layout_table(bool bf16, boo
                 : (to_hc ? &launch_layout<L, float2, float, true> : &launch_layout<L, float2, float, false>))...};
 }
 
-hipError_t launch_layout_convert(void* buf, int64_t rows, int logn, bool bf16, bool to_halfcomplex,
+hipError_t launch_layout_convert(void* buf, int64_t rows, int logn, bool half16, bool to_halfcomplex,
                                  hipStream_t stream) {
   static const auto seq = std::make_integer_sequence<int, kMaxLogN + 1>{};
   static const std::array<LayoutLauncher, kMaxLogN + 1> tables[4] = {
       make_layout_table(false, false, seq), make_layout_table(false, true, seq), make_layout_table(true, false, seq),
       make_layout_table(true, true, seq)};
-  return tables[(bf16 ? 2 : 0) + (to_halfcomplex ? 1 : 0)][logn](buf, rows, stream);
+  return tables[(half16 ? 2 : 0) + (to_halfcomplex ? 1 : 0)][logn](buf, rows, stream);
 }
 
 }  // namespace rdfft

@@ -15,8 +15,8 @@ __device__ __attribute__((aligned(16))) float2 g_twiddles[kTableEntries];
 
 // exchange rounds per pass of the row kernels
 template <int LOGN, class Acc>
-constexpr int row_chunks() {
-  return std::is_same<Acc, GlobalBF16>::value ? kChunksBf16[LOGN] : kChunks[LOGN];
+constexpr int row_chunks() {  // 16-bit storage: the bf16 table
+  return std::is_same<Acc, GlobalF32>::value ? kChunks[LOGN] : kChunksBf16[LOGN];
 }
 
 template <int LOGN, class Acc, class Elem, bool INV>
@@ -57,19 +57,19 @@ static hipError_t launch_rows(void* buf, int64_t rows, const float2* tw, hipStre
 
 using RowLauncher = hipError_t (*)(void*, int64_t, const float2*, hipStream_t, int);
 
-template <int... L>
-static std::array<RowLauncher, sizeof...(L)> make_row_table(bool bf16, bool inv, std::integer_sequence<int, L...>) {
-  return {(bf16 ? (inv ? &launch_rows<L, GlobalBF16, uint32_t, true> : &launch_rows<L, GlobalBF16, uint32_t, false>)
-                : (inv ? &launch_rows<L, GlobalF32, float2, true> : &launch_rows<L, GlobalF32, float2, false>))...};
+template <class Acc, class Elem, int... L>
+static std::array<RowLauncher, sizeof...(L)> make_row_table(bool inv, std::integer_sequence<int, L...>) {
+  return {(inv ? &launch_rows<L, Acc, Elem, true> : &launch_rows<L, Acc, Elem, false>)...};
 }
 
-hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, bool bf16, bool inv, const float2* tw,
+hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, int storage, bool inv, const float2* tw,
                              hipStream_t stream, int num_cu) {
   static const auto seq = std::make_integer_sequence<int, kMaxLogN + 1>{};
-  static const std::array<RowLauncher, kMaxLogN + 1> tables[4] = {
-      make_row_table(false, false, seq), make_row_table(false, true, seq), make_row_table(true, false, seq),
-      make_row_table(true, true, seq)};
-  return tables[(bf16 ? 2 : 0) + (inv ? 1 : 0)][logn](buf, rows, tw, stream, num_cu);
+  static const std::array<RowLauncher, kMaxLogN + 1> tables[3][2] = {
+      {make_row_table<GlobalF32, float2>(false, seq), make_row_table<GlobalF32, float2>(true, seq)},
+      {make_row_table<GlobalBF16, uint32_t>(false, seq), make_row_table<GlobalBF16, uint32_t>(true, seq)},
+      {make_row_table<GlobalF16, uint32_t>(false, seq), make_row_table<GlobalF16, uint32_t>(true, seq)}};
+  return tables[storage][inv ? 1 : 0][logn](buf, rows, tw, stream, num_cu);
 }
 
 hipError_t upload_twiddles(const void* host, size_t bytes, const float2** dev_ptr) {

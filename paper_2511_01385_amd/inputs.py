@@ -7,7 +7,9 @@ output without sharing any computation.
 
 Storage types: float32 arrays for ``"f32"``; for ``"bf16"`` the raw 16-bit
 patterns as ``uint16`` (round-to-nearest-even from the float32 value, the same
-rounding a bf16 store performs).  :func:`to_f64` widens either exactly.
+rounding a bf16 store performs); for ``"f16"`` IEEE half patterns as ``uint16``
+(NumPy's round-to-nearest-even conversion from float64).  :func:`to_f64` widens
+each exactly.
 
 Circulant parameters.  The paper's layers hold time-domain first columns
 c ~ N(0, sigma^2) and the library consumes their packed spectra.  For white
@@ -54,7 +56,9 @@ def _f32_to_bf16_bits(a32: np.ndarray) -> np.ndarray:
 
 
 def round_to(a: np.ndarray, dtype: str) -> np.ndarray:
-    """float64 values -> storage array of ``dtype`` ("f32" or "bf16")."""
+    """float64 values -> storage array of ``dtype`` ("f32", "bf16" or "f16")."""
+    if dtype == "f16":
+        return np.asarray(a, dtype=np.float64).astype(np.float16).view(np.uint16)
     a32 = np.asarray(a, dtype=np.float64).astype(np.float32)
     if dtype == "f32":
         return a32
@@ -70,6 +74,8 @@ def to_f64(stored: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         bits = np.asarray(stored, dtype=np.uint16).astype(np.uint32) << 16
         return bits.view(np.float32).astype(np.float64)
+    if dtype == "f16":
+        return np.asarray(stored, dtype=np.uint16).view(np.float16).astype(np.float64)
     raise ValueError(dtype)
 
 
@@ -79,7 +85,7 @@ def normal_rows(seed: int, rows: int, n: int, dtype: str, sigma: float = 1.0) ->
     Drawn in row-major order from one PCG64 stream, a block of rows at a time
     (the stream is consumed in the same order as by a single draw).
     """
-    if dtype not in ("f32", "bf16"):
+    if dtype not in ("f32", "bf16", "f16"):
         raise ValueError(dtype)
     g = generator(seed)
     out = np.empty((rows, n), dtype=np.float32 if dtype == "f32" else np.uint16)

@@ -74,9 +74,11 @@ def test_status_strings(lib):
         ((A, 4, 1, F32), EINVAL),
         ((A, 4, 0, F32), EINVAL),
         ((A, 4, -8, F32), EINVAL),
-        ((A, 4, 64, 2), EINVAL),  # unknown dtype
+        ((A, 4, 64, 3), EINVAL),  # unknown dtype
         ((A, 4, 96, F32), EUNSUP),  # even, not a power of two
         ((A, 4, 131072, BF16), EUNSUP),  # beyond 65536
+        ((A, 4, 131072, _lib.RDFFT_F16), EUNSUP),
+        ((A, 4, 6, _lib.RDFFT_F16), EUNSUP),
         ((A, 1 << 62, 65536, F32), EINVAL),  # size overflow
     ],
 )
@@ -91,6 +93,7 @@ def test_zero_rows_is_a_no_op(lib):
     assert lib.rdfft_inverse(None, 0, 4096, BF16, None) == OK
     assert lib.rdfft_pairs_to_halfcomplex(None, 0, 64, BF16, None) == OK
     assert lib.rdfft_halfcomplex_to_pairs(None, 0, 65536, F32, None) == OK
+    assert lib.rdfft_forward(None, 0, 2, _lib.RDFFT_F16, None) == OK
 
 
 def _grads(dx, dc):
@@ -108,6 +111,7 @@ def _grads(dx, dc):
         (A, B, A + (1 << 29), 256, 256, 64, -1, F32, EINVAL),
         (A, B, A + (1 << 29), 0, 256, 64, 8, F32, EINVAL),
         (A, B, A + (1 << 29), 256, 256, 64, 8, 5, EINVAL),
+        (A, B, A + (1 << 29), 256, 256, 64, 8, _lib.RDFFT_F16, EUNSUP),  # the layer stores f32 or bf16
         (0, B, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # null x
         (A, 0, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # null spectra
         (A, B, 0, 256, 256, 64, 8, F32, EINVAL),  # null y

@@ -19,7 +19,7 @@ from tests._helpers import assert_close, to_device, to_host_f64
 pytestmark = pytest.mark.gpu
 
 ALL_N = [2**k for k in range(1, 17)]
-DTYPES = ["f32", "bf16"]
+DTYPES = ["f32", "bf16", "f16"]
 
 
 def _rows_for(n):

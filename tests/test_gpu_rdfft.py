@@ -1,8 +1,9 @@
 """GPU parity of rdfft_forward / rdfft_inverse against the float64 oracle.
 
 Inputs come from the seeded generator; the reference is ``oracle.rdfft`` on the same
-stored values.  Covers every supported n (2 .. 65536), both storage types, row counts
-that span several workgroups with a ragged tail, the full batched-transform sizes
+stored values.  Covers every supported n (2 .. 65536), the three storage types
+(float32, bfloat16, float16), row counts that span several workgroups with a ragged
+tail, the full batched-transform sizes
 (2^16 rows for n = 64..4096; 1024 rows for n = 65536) on sampled rows, guard bands,
 run-to-run determinism and the absence of device allocation.
 """
@@ -13,12 +14,12 @@ import torch
 
 from oracle import rdfft as ord_
 from paper_2511_01385_amd import api, inputs
-from tests._helpers import assert_close, sample_rows, to_device, to_host_f64
+from tests._helpers import TORCH_DTYPE, assert_close, sample_rows, to_device, to_host_f64
 
 pytestmark = pytest.mark.gpu
 
 ALL_N = [2**k for k in range(1, 17)]
-DTYPES = ["f32", "bf16"]
+DTYPES = ["f32", "bf16", "f16"]
 
 
 def _rows_for(n):
@@ -129,7 +130,7 @@ def test_guard_bands_untouched(n, dtype):
     """Only the rows handed over are read and written."""
     rows, pad = 3 if n >= 16384 else 17, 4096
     x = inputs.normal_rows(_seed(n, dtype, 3), rows, n, dtype)
-    big = torch.full((pad + rows * n + pad,), float("nan"), dtype=torch.float32 if dtype == "f32" else torch.bfloat16,
+    big = torch.full((pad + rows * n + pad,), float("nan"), dtype=TORCH_DTYPE[dtype],
                      device="cuda")
     view = big[pad : pad + rows * n].view(rows, n)
     view.copy_(to_device(x, dtype))
@@ -138,20 +139,35 @@ def test_guard_bands_untouched(n, dtype):
     api.rdfft_inverse(view)
     torch.cuda.synchronize()
     assert torch.isnan(big[:pad]).all() and torch.isnan(big[pad + rows * n :]).all()
-    assert torch.equal(big[:pad].view(torch.int16 if dtype == "bf16" else torch.int32),
-                       before[:pad].view(torch.int16 if dtype == "bf16" else torch.int32))
+    assert torch.equal(big[:pad].view(torch.int32 if dtype == "f32" else torch.int16),
+                       before[:pad].view(torch.int32 if dtype == "f32" else torch.int16))
     assert np.isfinite(to_host_f64(view)).all()
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_zero_and_single_row(dtype):
-    t = torch.empty((0, 256), dtype=torch.float32 if dtype == "f32" else torch.bfloat16, device="cuda")
+    t = torch.empty((0, 256), dtype=TORCH_DTYPE[dtype], device="cuda")
     api.rdfft_forward(t)
     x = inputs.normal_rows(_seed(256, dtype, 4), 1, 256, dtype)
     t = to_device(x, dtype)
     api.rdfft_forward(t)
     torch.cuda.synchronize()
     assert_close(to_host_f64(t), ord_.rdfft_forward(inputs.to_f64(x, dtype)), dtype, "single row")
+
+
+@pytest.mark.parametrize("n", [1024, 65536])
+def test_f16_overflow_gives_infinity(n):
+    """float16 stores round to nearest: a DC bin of n = 65536 ones exceeds 65504 and becomes +inf.
+
+    The DC and Nyquist sums of integers are exact in float32; the other bins of a
+    constant row are zero up to the float32 rounding of the twiddle products."""
+    t = torch.ones((3, n), dtype=torch.float16, device="cuda")
+    api.rdfft_forward(t)
+    torch.cuda.synchronize()
+    got = t.float().cpu()
+    want_dc = float("inf") if n > 65504 else float(n)
+    assert (got[:, 0] == want_dc).all() and (got[:, 1] == 0).all()
+    assert (got[:, 2:].abs() < 1e-2).all()
 
 
 @pytest.mark.parametrize("n", [128, 4096, 65536])
