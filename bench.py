@@ -131,7 +131,8 @@ def config_table(dev, stream, reps: int = 10):
     Batched transforms for each n in 64..4096 (2^16 rows) in fp32 and bf16 storage and
     n = 65536 (1024 rows, fp32), forward and inverse, each over a rotating >= 1 GiB pool;
     and the three layer shapes (768-wide p = 256, 4096-wide p = 1024, 8192-wide p = 8192,
-    bf16, 4096 tokens) forward and backward.  GB/s are algorithmic bytes over the
+    bf16, 4096 tokens) and one 65536-wide circulant (p = 65536, bf16, 1024 tokens; the
+    multi-pass layer) forward and backward.  GB/s are algorithmic bytes over the
     event-timed average of `reps` back-to-back calls; frac is of 8 TB/s.
     """
     import torch
@@ -179,8 +180,8 @@ def config_table(dev, stream, reps: int = 10):
             "frac": round((gbs_f + gbs_i) / 2 / HBM_PEAK_GBS, 4)}
         del pool
     torch.cuda.empty_cache()
-    for d, p in ((768, 256), (4096, 1024), (8192, 8192)):
-        T = 4096
+    # the paper's three layer shapes, then one circulant beyond the fused kernels' blocks
+    for d, p, T in ((768, 256, 4096), (4096, 1024, 4096), (8192, 8192, 4096), (65536, 65536, 1024)):
         q = kb = d // p
         nset = max(2, -(-POOL_BYTES // (4 * T * d * 2)))
         sets = [dict(x=torch.randn(T, d, device=dev).to(torch.bfloat16),

@@ -96,7 +96,8 @@ def bca_forward(x: torch.Tensor, c_spectra: torch.Tensor, y: torch.Tensor) -> to
 def bca_backward(x: torch.Tensor, c_spectra: torch.Tensor, gy: torch.Tensor, dx: torch.Tensor, dc: torch.Tensor):
     """Writes dL/dx into ``dx`` and dL/dc (float32, time domain, shape (q, kb, p)) into ``dc``.
 
-    ``gy`` is left unspecified; ``dx`` may be ``gy`` itself when d_in == d_out.
+    ``gy`` is left unspecified; ``dx`` may be ``gy`` itself when d_in == d_out and p <= 8192
+    (longer blocks stage the input spectra in ``dx``).
     """
     q, kb, p = c_spectra.shape
     tokens = x.shape[0]

@@ -584,11 +584,19 @@ static hipError_t fwd_impl(const BcaArgs& a, const float2* tw, hipStream_t strea
   const size_t lds = (size_t)(TT * (a.kb + a.q) + 1) * region_bytes(LOGN);
   static const hipError_t attr = set_lds_limit(bca_forward_kernel<LOGN, Elem>);
   if (attr != hipSuccess) return attr;
-  const int64_t tiles = (a.tokens + TT - 1) / TT;
-  hipLaunchKernelGGL((bca_forward_kernel<LOGN, Elem>), dim3((unsigned)tiles), dim3(WG), lds, stream,
-                     static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<Elem*>(a.y), a.tokens,
-                     a.q, a.kb, TT, tw);
-  return hipGetLastError();
+  // one workgroup per tile, in launches within the grid limit
+  const int64_t per_launch = (kMaxGridThreads / WG) * TT;
+  constexpr int64_t N = (int64_t)1 << LOGN;
+  for (int64_t t0 = 0; t0 < a.tokens; t0 += per_launch) {
+    const int64_t nt = std::min<int64_t>(per_launch, a.tokens - t0);
+    const int64_t tiles = (nt + TT - 1) / TT;
+    hipLaunchKernelGGL((bca_forward_kernel<LOGN, Elem>), dim3((unsigned)tiles), dim3(WG), lds, stream,
+                       static_cast<const Elem*>(a.x) + t0 * a.kb * N, static_cast<const Elem*>(a.c),
+                       static_cast<Elem*>(a.y) + t0 * a.q * N, nt, a.q, a.kb, TT, tw);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // LDS of the backward's dC partial sums: q*kb*p/2 pair slots of float2
@@ -761,7 +769,8 @@ static std::array<BcaBwdFn, sizeof...(L)> bwd_table(bool bf16, std::integer_sequ
 
 bool bca_shape_supported(int logp, int q, int kb, bool backward) {
   const int logn = logp - 1;
-  if (logn < 0 || logn > kBcaMaxLogN) return false;
+  if (logn > kBcaMaxLogN) return bca_multipass_supported(logp, q, kb, backward);
+  if (logn < 0) return false;
   // one token's spectra must fit in LDS; the backward also needs room for the dC slots
   // of at least one block next to two spectra (block ranges cover the rest)
   if (tokens_per_tile(logn, kb, q, 1, 256, kLdsLimit) == 0) return false;
@@ -779,6 +788,7 @@ hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t st
        sq_fwd_table<4>(false, seq)},
       {sq_fwd_table<1>(true, seq), sq_fwd_table<2>(true, seq), sq_fwd_table<3>(true, seq),
        sq_fwd_table<4>(true, seq)}};
+  if (a.logp - 1 > kBcaMaxLogN) return launch_bca_multipass(a, false, tw, stream, num_cu);
   if (a.q == a.kb && a.q <= kSqMaxBlocks) {
     const BcaBwdFn fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
     if (fn != nullptr) return fn(a, tw, stream, num_cu);
@@ -797,10 +807,14 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
   static const std::array<BcaBwdFn, kBcaMaxLogN + 1> sq[2][kSqMaxBlocks] = {
       {sq_table<1>(false, seq), sq_table<2>(false, seq), sq_table<3>(false, seq), sq_table<4>(false, seq)},
       {sq_table<1>(true, seq), sq_table<2>(true, seq), sq_table<3>(true, seq), sq_table<4>(true, seq)}};
-  BcaBwdFn fn = nullptr;
-  if (a.q == a.kb && a.q <= kSqMaxBlocks) fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
-  if (fn == nullptr) fn = tab[a.bf16 ? 1 : 0][a.logp - 1];
-  e = fn(a, tw, stream, num_cu);
+  if (a.logp - 1 > kBcaMaxLogN) {
+    e = launch_bca_multipass(a, true, tw, stream, num_cu);
+  } else {
+    BcaBwdFn fn = nullptr;
+    if (a.q == a.kb && a.q <= kSqMaxBlocks) fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
+    if (fn == nullptr) fn = tab[a.bf16 ? 1 : 0][a.logp - 1];
+    e = fn(a, tw, stream, num_cu);
+  }
   if (e != hipSuccess) return e;
   // dc holds sum_t conj(X) . G as packed spectra; transform them in place to time domain
   return launch_rdfft_rows(a.dc, (int64_t)a.q * a.kb, a.logp - 1, kStorageF32, true, tw, stream, num_cu);

@@ -1,0 +1,319 @@
+// bca_multipass.hip -- the block-circulant layer for blocks too long for one workgroup's
+// LDS budget next to a second spectrum: 8192 < p <= 65536.
+//
+// The steps of Eqs. (4)-(5) run as separate passes over HBM.  The intermediate spectra
+// live in the caller's own output buffers, so the layer still needs no memory beyond
+// them:
+//   forward   X_tj = FFT(x_tj) into y's segment j (needs kb <= q), then per bin
+//             Y_ti = sum_j C_ij X_tj in place, then y_ti = IFFT(Y_ti) in place.  With
+//             q == kb == 1 the product is applied as the inverse transform loads.
+//   backward  G_ti = FFT(g_ti) in place in gy; X_tj = FFT(x_tj) into dx; per bin
+//             dC_ij = sum_t conj(X_tj) G_ti (float32 atomics into dc); per bin
+//             dX_tj = sum_i conj(C_ij) G_ti into dx; dx_tj = IFFT(dX_tj) in place; the
+//             caller's dc rows are then inverted like the fused path's.  With
+//             q == kb == 1 the dx product is applied as the inverse loads.
+// The intermediate spectra are stored in the layer's storage type (the in-place
+// transform keeps a spectrum in the storage of its input, Sec. 4.1); the arithmetic is
+// float32 throughout.
+#include <hip/hip_runtime.h>
+
+#include "fft_device.hpp"
+#include "launch.hpp"
+
+namespace rdfft {
+
+namespace {
+
+constexpr int kMpMinLogN = 13;  // p = 16384
+constexpr int kMpMaxLogN = 15;  // p = 65536
+constexpr int kMpMaxKb = 8;     // forward: input blocks held per bin
+
+// elementwise product of pair slot m with the matching slot of a spectrum w (times
+// conj(w) when CONJ); slot 0 holds the two real bins Y_0 and Y_{n/2}
+template <bool CONJ>
+__device__ __forceinline__ float2 slot_mul(int m, float2 a, float2 w) {
+  const float2 re = make_float2(a.x * w.x, a.y * w.y);
+  return m == 0 ? re : c_mul<CONJ>(a, w);
+}
+
+__device__ __forceinline__ float2 widen_slot(float2 v) { return v; }
+__device__ __forceinline__ float2 widen_slot(uint32_t v) { return bf16x2_to_f32(v); }
+template <class Elem>
+__device__ __forceinline__ Elem narrow_slot(float2 v);
+template <>
+__device__ __forceinline__ float2 narrow_slot<float2>(float2 v) {
+  return v;
+}
+template <>
+__device__ __forceinline__ uint32_t narrow_slot<uint32_t>(float2 v) {
+  return f32_to_bf16x2(v);
+}
+
+template <class Elem>
+struct StorageOf;
+template <>
+struct StorageOf<float2> {
+  using Acc = GlobalF32;
+  using Const = ConstF32;
+  static constexpr bool kHalf = false;
+};
+template <>
+struct StorageOf<uint32_t> {
+  using Acc = GlobalBF16;
+  using Const = ConstBF16;
+  static constexpr bool kHalf = true;
+};
+
+template <int LOGN, class Elem>
+constexpr int mp_chunks() {
+  return StorageOf<Elem>::kHalf ? kChunksBf16[LOGN] : kChunks[LOGN];
+}
+
+// Load accessor that returns the product of a stored spectrum slot with the matching
+// slot of one block spectrum (times its conjugate when CONJ)
+template <class GAcc, class CAcc, bool CONJ>
+struct MulLoad {
+  using raw_t = float2;
+  GAcc g;
+  CAcc c;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return r; }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return slot_mul<CONJ>(m, g.load(m), c.load(m)); }
+  __device__ __forceinline__ float2 load(int m) const { return load_raw(m); }
+};
+
+// Forward transform of rows r < rows of src into dst row (r / gin) * gout + r % gin
+// (src == dst with gin == gout is the in-place transform).
+template <int LOGN, class Elem>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
+    mp_forward_kernel(const Elem* src, Elem* dst, int64_t rows, int gin, int gout, const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, Elem>();
+  using P = RowPlan<LOGN, CH>;
+  static_assert(P::RW == 1, "one row per workgroup");
+  using S = StorageOf<Elem>;
+  __shared__ float2 lds[P::LDS_F2];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  if (row >= rows) return;  // whole workgroup: no barrier is skipped by part of it
+  const int64_t out_row = (row / gin) * gout + row % gin;
+  const typename S::Const in{src + row * (int64_t)P::N};
+  const typename S::Acc out{dst + out_row * (int64_t)P::N};
+  row_forward<LOGN, false, typename S::Const, typename S::Acc, CH>(t, true, in, out, lds, tw);
+}
+
+// dst row r = IFFT(spec . src row r), or IFFT(conj(spec) . src row r) when CONJ: the
+// last step of a single-block layer's forward (in place) and of its dx.  Every load of
+// a row precedes its first store, so src may be dst.
+template <int LOGN, class Elem, bool CONJ>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
+    mp_inverse_mul_kernel(const Elem* src, Elem* dst, const Elem* spec, int64_t rows, const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, Elem>();
+  using P = RowPlan<LOGN, CH>;
+  static_assert(P::RW == 1, "one row per workgroup");
+  using S = StorageOf<Elem>;
+  __shared__ float2 lds[P::LDS_F2];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  if (row >= rows) return;
+  const MulLoad<typename S::Const, typename S::Const, CONJ> in{typename S::Const{src + row * (int64_t)P::N},
+                                                              typename S::Const{spec}};
+  const typename S::Acc out{dst + row * (int64_t)P::N};
+  row_inverse<LOGN, false, decltype(in), typename S::Acc, CH>(t, true, in, out, lds, tw);
+}
+
+// Per bin, in place in y: Y_ti = sum_j C_ij X_tj, with X_tj in y's segment j (kb <= q).
+// One thread owns slot m of one token across all segments, so it reads every X_tj[m]
+// before it writes any Y_ti[m].
+template <class Elem>
+__global__ void __launch_bounds__(256) mp_fwd_product_kernel(Elem* y, const Elem* c, int64_t tokens, int q, int kb,
+                                                             int nslots, int xblocks) {
+  const int64_t b = blockIdx.x;
+  const int64_t tok = b / xblocks;
+  const int m = (int)(b - tok * xblocks) * 256 + threadIdx.x;
+  if (tok >= tokens || m >= nslots) return;
+  Elem* yt = y + tok * (int64_t)q * nslots;
+  float2 xv[kMpMaxKb];
+#pragma unroll
+  for (int j = 0; j < kMpMaxKb; ++j)
+    if (j < kb) xv[j] = widen_slot(yt[(int64_t)j * nslots + m]);
+  for (int i = 0; i < q; ++i) {
+    const Elem* ci = c + (int64_t)i * kb * nslots + m;
+    float2 acc = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int j = 0; j < kMpMaxKb; ++j)
+      if (j < kb) acc = c_add(acc, slot_mul<false>(m, xv[j], widen_slot(ci[(int64_t)j * nslots])));
+    yt[(int64_t)i * nslots + m] = narrow_slot<Elem>(acc);
+  }
+}
+
+// Per bin: dX_tj = sum_i conj(C_ij) G_ti into dx (G in gy).  Thread: slot m of (t, j).
+template <class Elem>
+__global__ void __launch_bounds__(256) mp_dx_product_kernel(const Elem* g, const Elem* c, Elem* dx, int64_t tokens,
+                                                            int q, int kb, int nslots, int xblocks) {
+  const int64_t b = blockIdx.x;
+  const int64_t row = b / xblocks;  // t * kb + j
+  const int m = (int)(b - row * xblocks) * 256 + threadIdx.x;
+  if (row >= tokens * kb || m >= nslots) return;
+  const int64_t tok = row / kb;
+  const int j = (int)(row - tok * kb);
+  const Elem* gt = g + tok * (int64_t)q * nslots + m;
+  const Elem* cj = c + (int64_t)j * nslots + m;
+  float2 acc = make_float2(0.f, 0.f);
+  for (int i = 0; i < q; ++i)
+    acc = c_add(acc, slot_mul<true>(m, widen_slot(gt[(int64_t)i * nslots]), widen_slot(cj[(int64_t)i * kb * nslots])));
+  dx[row * nslots + m] = narrow_slot<Elem>(acc);
+}
+
+// dC_ij[m] += sum_{t in chunk} conj(X_tj[m]) G_ti[m]; grid (slot blocks, q*kb, chunks).
+template <class Elem>
+__global__ void __launch_bounds__(256) mp_dc_kernel(const Elem* xs, const Elem* g, float* dc, int64_t tokens, int q,
+                                                    int kb, int nslots, int64_t tch) {
+  const int m = blockIdx.x * 256 + threadIdx.x;
+  if (m >= nslots) return;
+  const int pair = blockIdx.y;  // i * kb + j
+  const int i = pair / kb, j = pair - (pair / kb) * kb;
+  const int64_t t0 = (int64_t)blockIdx.z * tch;
+  const int64_t t1 = t0 + tch < tokens ? t0 + tch : tokens;
+  const Elem* xp = xs + (t0 * kb + j) * (int64_t)nslots + m;
+  const Elem* gp = g + (t0 * q + i) * (int64_t)nslots + m;
+  const int64_t xstep = (int64_t)kb * nslots, gstep = (int64_t)q * nslots;
+  float2 acc = make_float2(0.f, 0.f);
+#pragma unroll 8
+  for (int64_t tok = t0; tok < t1; ++tok, xp += xstep, gp += gstep)
+    acc = c_add(acc, slot_mul<true>(m, widen_slot(*gp), widen_slot(*xp)));
+  float* d = dc + 2 * ((int64_t)pair * nslots + m);
+  unsafeAtomicAdd(d, acc.x);
+  unsafeAtomicAdd(d + 1, acc.y);
+}
+
+// workgroups per launch: a dimension of the grid holds fewer than 2^32 work-items
+constexpr int64_t kMaxGrid256 = kMaxGridThreads / 256;
+
+template <int LOGN, class Elem>
+hipError_t forward_rows(const void* src, void* dst, int64_t rows, int gin, int gout, const float2* tw,
+                        hipStream_t stream) {
+  constexpr int N = 1 << LOGN;
+  using P = RowPlan<LOGN, mp_chunks<LOGN, Elem>()>;
+  const Elem* s = static_cast<const Elem*>(src);
+  Elem* d = static_cast<Elem*>(dst);
+  for (int64_t r0 = 0; r0 < rows;) {
+    const int64_t nr = std::min<int64_t>(rows - r0, kMaxGridThreads / P::WG);
+    // chunks start at a multiple of gin so the destination mapping restarts cleanly
+    const int64_t step = nr == rows - r0 ? nr : (nr / gin) * gin;
+    hipLaunchKernelGGL((mp_forward_kernel<LOGN, Elem>), dim3((unsigned)step), dim3(P::WG), 0, stream,
+                       s + r0 * (int64_t)N, d + (r0 / gin) * gout * (int64_t)N, step, gin, gout, tw);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    r0 += step;
+  }
+  return hipSuccess;
+}
+
+template <int LOGN, class Elem, bool CONJ>
+hipError_t inverse_mul_rows(const void* src, void* dst, const void* spec, int64_t rows, const float2* tw,
+                            hipStream_t stream) {
+  constexpr int N = 1 << LOGN;
+  using P = RowPlan<LOGN, mp_chunks<LOGN, Elem>()>;
+  for (int64_t r0 = 0; r0 < rows;) {
+    const int64_t nr = std::min<int64_t>(rows - r0, kMaxGridThreads / P::WG);
+    hipLaunchKernelGGL((mp_inverse_mul_kernel<LOGN, Elem, CONJ>), dim3((unsigned)nr), dim3(P::WG), 0, stream,
+                       static_cast<const Elem*>(src) + r0 * (int64_t)N, static_cast<Elem*>(dst) + r0 * (int64_t)N,
+                       static_cast<const Elem*>(spec), nr, tw);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    r0 += nr;
+  }
+  return hipSuccess;
+}
+
+// 1-D grid of (unit, block) pairs, `per` blocks per unit, in launches of at most
+// kMaxGrid256 blocks
+template <class F>
+hipError_t per_row_slots(int64_t nrows, int per, F launch) {
+  const int64_t rows_per = std::max<int64_t>(1, kMaxGrid256 / per);
+  for (int64_t r0 = 0; r0 < nrows; r0 += rows_per) {
+    const int64_t nr = std::min<int64_t>(rows_per, nrows - r0);
+    launch(r0, nr, (unsigned)(nr * per));
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+template <int LOGN, class Elem>
+hipError_t mp_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  constexpr int N = 1 << LOGN;
+  const int storage = StorageOf<Elem>::kHalf ? kStorageBF16 : kStorageF32;
+  const int64_t xrows = a.tokens * a.kb;
+  hipError_t e = forward_rows<LOGN, Elem>(a.x, a.y, xrows, a.kb, a.q, tw, stream);
+  if (e != hipSuccess) return e;
+  if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, Elem, false>(a.y, a.y, a.c, xrows, tw, stream);
+  const int xblocks = (N + 255) / 256;
+  Elem* y = static_cast<Elem*>(a.y);
+  e = per_row_slots(a.tokens, xblocks, [&](int64_t r0, int64_t nr, unsigned blocks) {
+    hipLaunchKernelGGL(mp_fwd_product_kernel<Elem>, dim3(blocks), dim3(256), 0, stream, y + r0 * (int64_t)a.q * N,
+                       static_cast<const Elem*>(a.c), nr, a.q, a.kb, N, xblocks);
+  });
+  if (e != hipSuccess) return e;
+  return launch_rdfft_rows(a.y, a.tokens * a.q, LOGN, storage, true, tw, stream, num_cu);
+}
+
+template <int LOGN, class Elem>
+hipError_t mp_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  constexpr int N = 1 << LOGN;
+  const int storage = StorageOf<Elem>::kHalf ? kStorageBF16 : kStorageF32;
+  const int64_t grows = a.tokens * a.q, xrows = a.tokens * a.kb;
+  // G = FFT(g) in place; X = FFT(x) into dx
+  hipError_t e = launch_rdfft_rows(a.y, grows, LOGN, storage, false, tw, stream, num_cu);
+  if (e != hipSuccess) return e;
+  e = forward_rows<LOGN, Elem>(a.x, a.dx, xrows, 1, 1, tw, stream);
+  if (e != hipSuccess) return e;
+  // dC: slot blocks x pairs x token chunks, about 2048 workgroups in all (q * kb <= 65535)
+  const int xblocks = (N + 255) / 256;
+  const int pairs = a.q * a.kb;
+  int64_t chunks = std::max<int64_t>(1, 2048 / ((int64_t)xblocks * pairs));
+  chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, a.tokens / 16));
+  int64_t tch = std::max<int64_t>((a.tokens + chunks - 1) / chunks, (a.tokens + 65534) / 65535);
+  chunks = (a.tokens + tch - 1) / tch;
+  hipLaunchKernelGGL(mp_dc_kernel<Elem>, dim3(xblocks, pairs, (unsigned)chunks), dim3(256), 0, stream,
+                     static_cast<const Elem*>(a.dx), static_cast<const Elem*>(a.y), a.dc, a.tokens, a.q, a.kb, N,
+                     tch);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, Elem, true>(a.y, a.dx, a.c, xrows, tw, stream);
+  // dX into dx, then its inverse in place; launches cover whole tokens
+  Elem* dx = static_cast<Elem*>(a.dx);
+  e = per_row_slots(a.tokens, xblocks * a.kb, [&](int64_t t0, int64_t nt, unsigned blocks) {
+    hipLaunchKernelGGL(mp_dx_product_kernel<Elem>, dim3(blocks), dim3(256), 0, stream,
+                       static_cast<const Elem*>(a.y) + t0 * a.q * (int64_t)N, static_cast<const Elem*>(a.c),
+                       dx + t0 * a.kb * (int64_t)N, nt, a.q, a.kb, N, xblocks);
+  });
+  if (e != hipSuccess) return e;
+  return launch_rdfft_rows(a.dx, xrows, LOGN, storage, true, tw, stream, num_cu);
+}
+
+using MpFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t, int);
+
+template <int... L>
+std::array<MpFn, sizeof...(L)> mp_table(bool bf16, bool backward, std::integer_sequence<int, L...>) {
+  return {(backward ? (bf16 ? &mp_backward<L + kMpMinLogN, uint32_t> : &mp_backward<L + kMpMinLogN, float2>)
+                    : (bf16 ? &mp_forward<L + kMpMinLogN, uint32_t> : &mp_forward<L + kMpMinLogN, float2>))...};
+}
+
+}  // namespace
+
+bool bca_multipass_supported(int logp, int q, int kb, bool backward) {
+  const int logn = logp - 1;
+  if (logn < kMpMinLogN || logn > kMpMaxLogN) return false;
+  if ((int64_t)q * kb > 65535) return false;  // the dC grid's second dimension
+  if (backward) return true;
+  return kb <= q && kb <= kMpMaxKb;
+}
+
+hipError_t launch_bca_multipass(const BcaArgs& a, bool backward, const float2* tw, hipStream_t stream, int num_cu) {
+  static const auto seq = std::make_integer_sequence<int, kMpMaxLogN - kMpMinLogN + 1>{};
+  static const std::array<MpFn, kMpMaxLogN - kMpMinLogN + 1> tab[2][2] = {
+      {mp_table(false, false, seq), mp_table(true, false, seq)}, {mp_table(false, true, seq), mp_table(true, true, seq)}};
+  return tab[backward ? 1 : 0][a.bf16 ? 1 : 0][a.logp - 1 - kMpMinLogN](a, tw, stream, num_cu);
+}
+
+}  // namespace rdfft

@@ -207,6 +207,8 @@ int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* gr
     if (overlaps(dx, sh.x_bytes, x, sh.x_bytes) || overlaps(dx, sh.x_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
     if (dx == gy) {
       if (d_in != d_out) return RDFFT_EINVAL;
+      // blocks beyond 8192 stage the input spectra in dx while gy holds the upstream ones
+      if (p > 8192) return RDFFT_EUNSUPPORTED;
     } else if (overlaps(dx, sh.x_bytes, gy, sh.y_bytes)) {
       return RDFFT_EINVAL;
     }

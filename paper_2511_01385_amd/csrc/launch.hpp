@@ -13,6 +13,10 @@ namespace rdfft {
 // Storage types of the row kernels (the values of rdfft_dtype_t)
 constexpr int kStorageF32 = 0, kStorageBF16 = 1, kStorageF16 = 2;
 
+// Work-items per launch: each grid dimension holds fewer than 2^32 of them, so launches
+// are split to stay at or below this.
+constexpr int64_t kMaxGridThreads = (int64_t)1 << 31;
+
 // In-place forward (inv = false) or inverse rdFFT of `rows` rows of 2^(logn+1) elements
 // (rows >= 1) stored as `storage`.
 hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, int storage, bool inv, const float2* tw,
@@ -43,5 +47,12 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
 
 // whether the fused forward (or backward) kernel handles p = 2^logp with q x kb blocks
 bool bca_shape_supported(int logp, int q, int kb, bool backward);
+
+// The multi-pass layer for 8192 < p <= 65536 (bca_multipass.hip).  The forward needs
+// kb <= q (the input spectra are staged in y); the backward needs dx distinct from gy
+// (the input spectra are staged in dx while gy holds the upstream spectra).  The
+// backward launcher expects dc zeroed and leaves it as packed spectra.
+bool bca_multipass_supported(int logp, int q, int kb, bool backward);
+hipError_t launch_bca_multipass(const BcaArgs& a, bool backward, const float2* tw, hipStream_t stream, int num_cu);
 
 }  // namespace rdfft

@@ -80,7 +80,7 @@ struct alignas(4) U16x2 {
 template <int LOGN, class Pair, class Scalar, bool TO_HC>
 static hipError_t launch_layout(void* buf, int64_t rows, hipStream_t stream) {
   using L = LayoutPlan<LOGN>;
-  const int64_t max_blocks = (int64_t)1 << 30;
+  const int64_t max_blocks = kMaxGridThreads / L::WG;
   Scalar* base = static_cast<Scalar*>(buf);
   for (int64_t r0 = 0; r0 < rows;) {
     const int64_t blocks = std::min<int64_t>((rows - r0 + L::RW - 1) / L::RW, max_blocks);

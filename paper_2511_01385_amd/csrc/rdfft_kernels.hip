@@ -41,7 +41,7 @@ template <int LOGN, class Acc, class Elem, bool INV>
 static hipError_t launch_rows(void* buf, int64_t rows, const float2* tw, hipStream_t stream, int) {
   using P = RowPlan<LOGN>;
   // keep every launch within the grid limit
-  const int64_t max_blocks = (int64_t)1 << 30;
+  const int64_t max_blocks = kMaxGridThreads / P::WG;
   Elem* base = static_cast<Elem*>(buf);
   for (int64_t r0 = 0; r0 < rows;) {
     const int64_t blocks = std::min<int64_t>((rows - r0 + P::RW - 1) / P::RW, max_blocks);

@@ -8,6 +8,13 @@ Comparison rule (both must hold):
 * element by element, |gpu - ref| <= 2^-8 |ref| (bf16) or 2^-11 |ref| (f16): one
   round-to-nearest-even store, + 2e-5 * rms(ref of that row) (float32 arithmetic).
 
+Outputs that pass through `staged` spectra stored in a 16-bit type on the way (the
+layer for blocks beyond 8192 keeps its intermediate spectra in the storage type) widen
+the element bound by 4 sqrt(staged) u rms(row), u = 2^-8 (bf16): a rounding of a spectrum
+spreads over every element of the row after the inverse transform, with an RMS of about
+u / (2 sqrt 3) of the row's, and the largest of many millions of such errors reaches about
+six times that.
+
 For f16 storage the rel-L2 bound is 2e-3: one store rounding contributes at most
 2^-12 relative RMS (2.4e-4) and the float32 arithmetic ~1e-7, so 2e-3 keeps an 8x
 margin while still failing on any mistake larger than the storage resolution.
@@ -48,7 +55,7 @@ def rel_l2(got: np.ndarray, ref: np.ndarray) -> float:
     return float(np.linalg.norm(got - ref) / (den if den > 0 else 1.0))
 
 
-def assert_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "") -> float:
+def assert_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "", staged: int = 0) -> float:
     got = np.asarray(got, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     assert got.shape == ref.shape, (got.shape, ref.shape)
@@ -58,7 +65,7 @@ def assert_close(got: np.ndarray, ref: np.ndarray, dtype: str, what: str = "") -
     r2 = ref.reshape(-1, ref.shape[-1]) if ref.ndim > 1 else ref.reshape(1, -1)
     g2 = got.reshape(r2.shape)
     rms = np.sqrt(np.mean(r2**2, axis=1, keepdims=True))
-    bound = 2e-5 * rms + ELEMENT_REL[dtype] * np.abs(r2)
+    bound = (2e-5 + 4 * np.sqrt(staged) * ELEMENT_REL[dtype]) * rms + ELEMENT_REL[dtype] * np.abs(r2)
     bad = np.abs(g2 - r2) > bound
     if bad.any():
         i, j = np.argwhere(bad)[0]

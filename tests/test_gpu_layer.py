@@ -27,7 +27,8 @@ def _oracle_spectra(c: torch.Tensor, dtype: str) -> np.ndarray:
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("d_in,d_out,p,lead", [(256, 256, 64, (3, 5)), (512, 1024, 128, (7,)), (768, 256, 256, (2, 3))])
+@pytest.mark.parametrize("d_in,d_out,p,lead", [(256, 256, 64, (3, 5)), (512, 1024, 128, (7,)), (768, 256, 256, (2, 3)),
+                                               (16384, 16384, 16384, (2, 2))])
 def test_forward_backward_match_oracle(dtype, d_in, d_out, p, lead):
     torch.manual_seed(d_in + d_out + p)
     layer = BlockCirculantLinear(d_in, d_out, p, dtype=TORCH_DTYPE[dtype])
@@ -45,10 +46,13 @@ def test_forward_backward_match_oracle(dtype, d_in, d_out, p, lead):
     xf, gf = inputs.to_f64(x_st, dtype), inputs.to_f64(g_st, dtype)
     y_ref = obca.forward_spectral(xf, spec, d_out, p)
     dx_ref, dc_ref = obca.backward_spectral(xf, spec, gf, p)
-    assert_close(to_host_f64(y.reshape(-1, d_out)), y_ref, dtype, "y")
-    assert_close(to_host_f64(x.grad.reshape(-1, d_in)), dx_ref, dtype, "dx")
+    staged = 2 if p > 8192 else 0  # long blocks store their intermediate spectra
+    assert_close(to_host_f64(y.reshape(-1, d_out)), y_ref, dtype, "y", staged)
+    assert_close(to_host_f64(x.grad.reshape(-1, d_in)), dx_ref, dtype, "dx", staged)
     assert layer.c.grad.dtype == torch.float32
-    assert_close(layer.c.grad.double().cpu().numpy().reshape(-1, p), dc_ref.reshape(-1, p), "f32", "dc")
+    # long blocks keep a bf16 layer's intermediate spectra in bf16: dc meets the bf16 bar
+    dc_bar = "bf16" if dtype == "bf16" and p > 8192 else "f32"
+    assert_close(layer.c.grad.double().cpu().numpy().reshape(-1, p), dc_ref.reshape(-1, p), dc_bar, "dc", staged)
 
 
 def test_clobber_grad_reuses_the_upstream_gradient():
