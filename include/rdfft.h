@@ -60,7 +60,8 @@ typedef enum {
 typedef enum {
   RDFFT_OK = 0,
   RDFFT_EINVAL = -1,       /* invalid argument (null/misaligned pointer, bad size, overlap) */
-  RDFFT_EUNSUPPORTED = -2, /* valid but not implemented (n > 65536, non power-of-two n, p > 8192) */
+  RDFFT_EUNSUPPORTED = -2, /* valid but not implemented (n > 65536, non power-of-two n, p > 65536,
+                              and the long-block limits of bca_forward / bca_backward) */
   RDFFT_ELAUNCH = -3,      /* HIP reported an error when enqueuing */
   RDFFT_EDEVICE = -4       /* no usable gfx950 device, or the twiddle table upload failed */
 } rdfft_status_t;
@@ -123,9 +124,12 @@ typedef struct {
  *              overlap with x or c_spectra -> RDFFT_EINVAL.
  *   grads      reserved, must be NULL.
  *   dtype      RDFFT_F32 or RDFFT_BF16 (RDFFT_F16 -> RDFFT_EUNSUPPORTED).
- *   p          power of two, 2 <= p <= 8192 (larger -> RDFFT_EUNSUPPORTED);
+ *   p          power of two, 2 <= p <= 65536 (larger -> RDFFT_EUNSUPPORTED);
  *              must divide d_in and d_out (Table 1 marks such shapes N/A) -> else RDFFT_EINVAL.
  *   tokens     >= 0; 0 is a no-op (x and y may then be NULL).
+ * Blocks beyond 8192 (p = 16384, 32768, 65536) run as passes over HBM that stage the
+ * input spectra in y: they need kb <= q and kb <= 8 (else RDFFT_EUNSUPPORTED), and the
+ * staged spectra are stored in dtype (for bf16 one more rounding of each spectrum).
  */
 RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_grads_t *grads, int64_t d_in,
                 int64_t d_out, int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream);
@@ -140,7 +144,10 @@ RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_gra
  *   gy         [tokens][d_out] in dtype: the upstream gradient.  Its contents
  *              are unspecified on return (the layer may use it as work space,
  *              Sec. 5.1.1 "overwriting the grad_output").
- *   grads->dx  [tokens][d_in] in dtype, written; may equal gy when d_in == d_out.
+ *   grads->dx  [tokens][d_in] in dtype, written; may equal gy when d_in == d_out and
+ *              p <= 8192.  Blocks beyond 8192 stage the input spectra in dx while gy
+ *              holds the upstream ones: dx == gy -> RDFFT_EUNSUPPORTED, and q * kb must
+ *              not exceed 65535.
  *   grads->dc  [q][kb][p] float32, written (overwritten, not accumulated).
  *              Summed with float32 atomics, so the last bits may vary run to run.
  *   Other arguments as bca_forward.  tokens == 0 writes dc = 0.
