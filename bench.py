@@ -128,8 +128,9 @@ def cpu_baseline(host_rows, host_bca, min_seconds: float = 10.0):
 def config_table(dev, stream, reps: int = 10):
     """Untimed-by-`value` context: every workload shape of the paper's configurations.
 
-    Batched transforms for each n in 64..4096 (2^16 rows) in fp32 and bf16 storage and
-    n = 65536 (1024 rows, fp32), forward and inverse, each over a rotating >= 1 GiB pool;
+    Batched transforms for each n in 64..4096 (2^16 rows) in fp32 and bf16 storage,
+    n = 65536 (1024 rows, fp32) and the mixed-radix lengths n = 3000 (fp32) and n = 6144
+    (bf16, 2^16 rows each), forward and inverse, each over a rotating >= 1 GiB pool;
     and the three layer shapes (768-wide p = 256, 4096-wide p = 1024, 8192-wide p = 8192,
     bf16, 4096 tokens) and one 65536-wide circulant (p = 65536, bf16, 1024 tokens; the
     multi-pass layer) forward and backward.  GB/s are algorithmic bytes over the
@@ -151,7 +152,9 @@ def config_table(dev, stream, reps: int = 10):
         return e0.elapsed_time(e1) * 1e3 / reps
 
     table = {}
+    # the batched-transform sizes, the longest rows, and two mixed-radix lengths
     shapes = [(n, ROWS, dt) for dt in ("f32", "bf16") for n in NS] + [(65536, 1024, "f32")]
+    shapes += [(3000, ROWS, "f32"), (6144, ROWS, "bf16")]
     for n, rows, dt in shapes:
         tdt = torch.float32 if dt == "f32" else torch.bfloat16
         nb = rows * n * (4 if dt == "f32" else 2)

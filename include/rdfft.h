@@ -60,7 +60,8 @@ typedef enum {
 typedef enum {
   RDFFT_OK = 0,
   RDFFT_EINVAL = -1,       /* invalid argument (null/misaligned pointer, bad size, overlap) */
-  RDFFT_EUNSUPPORTED = -2, /* valid but not implemented (n > 65536, non power-of-two n, p > 65536,
+  RDFFT_EUNSUPPORTED = -2, /* valid but not implemented (n > 65536, n/2 with a prime factor
+                              above 5 or beyond 16384 when not a power of two, p > 65536,
                               and the long-block limits of bca_forward / bca_backward) */
   RDFFT_ELAUNCH = -3,      /* HIP reported an error when enqueuing */
   RDFFT_EDEVICE = -4       /* no usable gfx950 device, or the twiddle table upload failed */
@@ -73,8 +74,10 @@ typedef enum {
  *         real samples x_0..x_{n-1} of each row; on return the packed spectrum
  *         of that row in the layout above.
  *   rows  >= 0; rows == 0 is a no-op (buf may then be NULL).
- *   n     power of two, 2 <= n <= 65536.  Odd n -> RDFFT_EINVAL (no Nyquist
- *         bin, Theorem 1); even non-power-of-two or n > 65536 -> RDFFT_EUNSUPPORTED.
+ *   n     even, 2 <= n: a power of two up to 65536, or n = 2N with N = 2^a 3^b 5^c
+ *         up to 16384 (mixed-radix rows: one workgroup per row, the row in LDS,
+ *         twiddles from sincospi).  Odd n -> RDFFT_EINVAL (no Nyquist bin,
+ *         Theorem 1); any other even n -> RDFFT_EUNSUPPORTED.
  * No memory beyond buf is read or written (apart from the twiddle table).
  */
 RDFFT_API int rdfft_forward(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);

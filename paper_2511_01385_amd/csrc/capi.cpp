@@ -83,7 +83,8 @@ int check_transform(const void* buf, int64_t rows, int64_t n, int dtype) {
   if (dtype != RDFFT_F32 && dtype != RDFFT_BF16 && dtype != RDFFT_F16) return RDFFT_EINVAL;
   if (rows < 0) return RDFFT_EINVAL;
   if (n < 2 || (n & 1)) return RDFFT_EINVAL;
-  if (!is_pow2(n) || n > (int64_t(2) << rdfft::kMaxLogN)) return RDFFT_EUNSUPPORTED;
+  if (is_pow2(n) ? n > (int64_t(2) << rdfft::kMaxLogN) : !rdfft::mixed_length_supported(n))
+    return RDFFT_EUNSUPPORTED;
   if (rows == 0) return RDFFT_OK;
   int64_t count = 0, bytes = 0;
   if (!mul_ok(rows, n, &count) || !mul_ok(count, elem_bytes(dtype), &bytes)) return RDFFT_EINVAL;
@@ -98,8 +99,9 @@ int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stre
   int num_cu = 0;
   st = ensure_device(&tw, &num_cu);
   if (st != RDFFT_OK) return st;
-  const hipError_t e = rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype, inv, tw,
-                                                reinterpret_cast<hipStream_t>(stream), num_cu);
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = is_pow2(n) ? rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype, inv, tw, s, num_cu)
+                                  : rdfft::launch_mixed_rows(buf, rows, n, dtype, inv, s);
   return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
 }
 
@@ -110,8 +112,9 @@ int convert(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream
   const float2* tw = nullptr;
   st = ensure_device(&tw, nullptr);
   if (st != RDFFT_OK) return st;
-  const hipError_t e = rdfft::launch_layout_convert(buf, rows, ilog2(n) - 1, dtype != RDFFT_F32, to_hc,
-                                                    reinterpret_cast<hipStream_t>(stream));
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const hipError_t e = is_pow2(n) ? rdfft::launch_layout_convert(buf, rows, ilog2(n) - 1, dtype != RDFFT_F32, to_hc, s)
+                                  : rdfft::launch_mixed_layout(buf, rows, n, dtype != RDFFT_F32, to_hc, s);
   return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
 }
 

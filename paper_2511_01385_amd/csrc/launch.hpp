@@ -27,6 +27,14 @@ hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, int storage, boo
 hipError_t launch_layout_convert(void* buf, int64_t rows, int logn, bool half16, bool to_halfcomplex,
                                  hipStream_t stream);
 
+// Rows whose half-length N = n/2 is 2^a 3^b 5^c but not a power of two, N <= 16384
+// (mixed_kernels.hip): the transforms and the layout converters, rows >= 1.
+constexpr int64_t kMixedMaxHalf = 16384;
+bool mixed_length_supported(int64_t n);
+hipError_t launch_mixed_rows(void* buf, int64_t rows, int64_t n, int storage, bool inv, hipStream_t stream);
+hipError_t launch_mixed_layout(void* buf, int64_t rows, int64_t n, bool half16, bool to_halfcomplex,
+                               hipStream_t stream);
+
 // Copies the host twiddle table to the current device; returns its device address.
 hipError_t upload_twiddles(const void* host, size_t bytes, const float2** dev_ptr);
 

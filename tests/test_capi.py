@@ -75,10 +75,12 @@ def test_status_strings(lib):
         ((A, 4, 0, F32), EINVAL),
         ((A, 4, -8, F32), EINVAL),
         ((A, 4, 64, 3), EINVAL),  # unknown dtype
-        ((A, 4, 96, F32), EUNSUP),  # even, not a power of two
+        ((A, 4, 14, F32), EUNSUP),  # even, n/2 has a factor 7
+        ((A, 4, 49152, F32), EUNSUP),  # n/2 = 3 * 2^13: mixed radix beyond 16384
+        ((A, 4, 2 * 3**10, F32), EUNSUP),
         ((A, 4, 131072, BF16), EUNSUP),  # beyond 65536
         ((A, 4, 131072, _lib.RDFFT_F16), EUNSUP),
-        ((A, 4, 6, _lib.RDFFT_F16), EUNSUP),
+        ((A, 4, 22, _lib.RDFFT_F16), EUNSUP),
         ((A, 1 << 62, 65536, F32), EINVAL),  # size overflow
     ],
 )
@@ -94,6 +96,7 @@ def test_zero_rows_is_a_no_op(lib):
     assert lib.rdfft_pairs_to_halfcomplex(None, 0, 64, BF16, None) == OK
     assert lib.rdfft_halfcomplex_to_pairs(None, 0, 65536, F32, None) == OK
     assert lib.rdfft_forward(None, 0, 2, _lib.RDFFT_F16, None) == OK
+    assert lib.rdfft_inverse(None, 0, 30000, BF16, None) == OK  # mixed radix
 
 
 def _grads(dx, dc):

@@ -49,6 +49,22 @@ def test_pairs_to_halfcomplex_bit_exact(n, dtype):
 
 
 @pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("n", [6, 30, 96, 1000, 12288, 32000])
+def test_mixed_lengths_bit_exact(n, dtype):
+    """Rows whose half-length has factors 3 and 5 use the same permutation."""
+    rows = 31 if n <= 1000 else 3
+    y = inputs.normal_rows(7373 + n, rows, n, dtype)
+    t = to_device(y, dtype)
+    api.rdfft_pairs_to_halfcomplex(t)
+    torch.cuda.synchronize()
+    want = inputs.round_to(ord_.pack_halfcomplex(ord_.unpack_pairs(inputs.to_f64(y, dtype))), dtype)
+    assert np.array_equal(_bits(t), _bits(to_device(want, dtype)))
+    api.rdfft_halfcomplex_to_pairs(t)
+    torch.cuda.synchronize()
+    assert np.array_equal(_bits(t), _bits(to_device(y, dtype)))
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
 @pytest.mark.parametrize("n", [16, 1024, 65536])
 def test_halfcomplex_to_pairs_bit_exact(n, dtype):
     rows = _rows_for(n)
@@ -89,4 +105,4 @@ def test_zero_rows_and_errors():
     t = torch.zeros(0, 64, device="cuda")
     api.rdfft_pairs_to_halfcomplex(t)
     with pytest.raises(api.RdfftError):
-        api.rdfft_pairs_to_halfcomplex(torch.zeros(3, 96, device="cuda"))
+        api.rdfft_pairs_to_halfcomplex(torch.zeros(3, 14, device="cuda"))  # n/2 = 7: no plan

@@ -5,7 +5,8 @@ stored values.  Covers every supported n (2 .. 65536), the three storage types
 (float32, bfloat16, float16), row counts that span several workgroups with a ragged
 tail, the full batched-transform sizes
 (2^16 rows for n = 64..4096; 1024 rows for n = 65536) on sampled rows, guard bands,
-run-to-run determinism and the absence of device allocation.
+run-to-run determinism and the absence of device allocation; and the mixed-radix rows
+(n/2 = 2^a 3^b 5^c, not a power of two, up to 16384) in every storage type.
 """
 
 import numpy as np
@@ -168,6 +169,41 @@ def test_f16_overflow_gives_infinity(n):
     want_dc = float("inf") if n > 65504 else float(n)
     assert (got[:, 0] == want_dc).all() and (got[:, 1] == 0).all()
     assert (got[:, 2:].abs() < 1e-2).all()
+
+
+# even lengths whose half is 2^a 3^b 5^c but not a power of two: the mixed-radix rows
+MIXED_N = [6, 10, 12, 30, 48, 96, 120, 360, 1000, 3000, 6144, 12288, 30000, 32000]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("n", MIXED_N)
+def test_mixed_radix_parity(n, dtype):
+    rows = 257 if n <= 3000 else 9
+    x = inputs.normal_rows(_seed(n, dtype, 6), rows, n, dtype)
+    t = to_device(x, dtype)
+    api.rdfft_forward(t)
+    torch.cuda.synchronize()
+    assert_close(to_host_f64(t), ord_.rdfft_forward(inputs.to_f64(x, dtype)), dtype, f"mixed forward n={n} {dtype}")
+    y = inputs.normal_rows(_seed(n, dtype, 7), rows, n, dtype)
+    t = to_device(y, dtype)
+    api.rdfft_inverse(t)
+    torch.cuda.synchronize()
+    assert_close(to_host_f64(t), ord_.rdfft_inverse(inputs.to_f64(y, dtype)), dtype, f"mixed inverse n={n} {dtype}")
+
+
+@pytest.mark.parametrize("n", [30, 3000, 32000])
+def test_mixed_radix_guard_bands_and_round_trip(n):
+    rows, pad = 5, 1024
+    x = inputs.normal_rows(_seed(n, "f32", 8), rows, n, "f32")
+    big = torch.full((pad + rows * n + pad,), float("nan"), device="cuda")
+    view = big[pad : pad + rows * n].view(rows, n)
+    view.copy_(to_device(x, "f32"))
+    api.rdfft_forward(view)
+    api.rdfft_inverse(view)
+    torch.cuda.synchronize()
+    assert torch.isnan(big[:pad]).all() and torch.isnan(big[pad + rows * n :]).all()
+    back = to_host_f64(view)
+    assert np.linalg.norm(back - x) / np.linalg.norm(x) < 2e-6
 
 
 @pytest.mark.parametrize("n", [128, 4096, 65536])

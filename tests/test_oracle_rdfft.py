@@ -19,6 +19,8 @@ from oracle import rdfft as rd
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 METHODS = ["direct", "fft"]
 SIZES = [2, 4, 8, 16, 64, 256, 1024]
+# even lengths whose half has factors 3 and 5 (the mixed-radix rows)
+MIXED = [6, 10, 12, 30, 48, 90, 750]
 
 
 def _read_golden(name):
@@ -44,7 +46,7 @@ def test_golden_worked_examples(name, method):
 
 
 @pytest.mark.parametrize("method", METHODS)
-@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("n", SIZES + MIXED)
 def test_closed_forms(n, method):
     m = np.arange(n)
     # unit impulse -> every bin is 1
@@ -86,7 +88,7 @@ def test_closed_forms(n, method):
 
 
 @pytest.mark.parametrize("method", METHODS)
-@pytest.mark.parametrize("n", [4, 8, 64, 512])
+@pytest.mark.parametrize("n", [4, 8, 64, 512, 6, 30, 90])
 def test_inverse_of_unit_slots(n, method):
     """Each packed slot's inverse is a known real sinusoid (Eq. (1) with Y_{n-k} = conj Y_k)."""
     m = np.arange(n)
@@ -99,7 +101,7 @@ def test_inverse_of_unit_slots(n, method):
         np.testing.assert_allclose(x[2 * k + 1], -2 * np.sin(2 * np.pi * k * m / n) / n, atol=1e-13)
 
 
-@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("n", SIZES + MIXED)
 def test_theorem1_and_parseval(n):
     rng = np.random.default_rng(n)
     x = rng.standard_normal((3, n))
@@ -134,7 +136,7 @@ def test_linearity_and_shift(n, method):
 
 @pytest.mark.parametrize("layout", ["pairs", "halfcomplex"])
 @pytest.mark.parametrize("method", METHODS)
-@pytest.mark.parametrize("n", SIZES)
+@pytest.mark.parametrize("n", SIZES + MIXED)
 def test_round_trip_both_ways(n, method, layout):
     rng = np.random.default_rng(100 + n)
     x = rng.standard_normal((4, n))
@@ -143,7 +145,7 @@ def test_round_trip_both_ways(n, method, layout):
     np.testing.assert_allclose(rd.rdfft_forward(rd.rdfft_inverse(buf, method, layout), method, layout), buf, atol=1e-11)
 
 
-@pytest.mark.parametrize("n", [2, 4, 16, 128, 1024])
+@pytest.mark.parametrize("n", [2, 4, 16, 128, 1024] + MIXED)
 def test_direct_definition_pins_library_route(n):
     rng = np.random.default_rng(3 * n)
     x = rng.standard_normal((5, n))
