@@ -106,3 +106,21 @@ def test_zero_rows_and_errors():
     api.rdfft_pairs_to_halfcomplex(t)
     with pytest.raises(api.RdfftError):
         api.rdfft_pairs_to_halfcomplex(torch.zeros(3, 14, device="cuda"))  # n/2 = 7: no plan
+
+
+def test_launch_split_beyond_grid_limit_mixed():
+    """2^25 + 7 rows of n = 6: more rows than one launch of 64-thread workgroups holds."""
+    rows = (1 << 25) + 7
+    r = torch.arange(rows, device="cuda", dtype=torch.int64) % 1000
+    t = (r[:, None].float() + torch.arange(6, device="cuda").float()[None, :] / 8).contiguous()
+    orig = t.clone()
+    api.rdfft_pairs_to_halfcomplex(t)
+    torch.cuda.synchronize()
+    # pair slot k -> real slots (k, n - k), slot 0 -> (0, n/2): [s0, s2, s4, s1, s5, s3]
+    perm = torch.as_tensor([0, 2, 4, 1, 5, 3], device="cuda")
+    assert torch.equal(t, orig[:, perm])
+    api.rdfft_halfcomplex_to_pairs(t)
+    torch.cuda.synchronize()
+    assert torch.equal(t, orig)
+    del t, orig, r
+    torch.cuda.empty_cache()

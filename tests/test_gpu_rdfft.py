@@ -206,6 +206,48 @@ def test_mixed_radix_guard_bands_and_round_trip(n):
     assert np.linalg.norm(back - x) / np.linalg.norm(x) < 2e-6
 
 
+def _split_rows_check(t, n, dtype, rows_checked, what):
+    """Forward then inverse over a buffer whose launches are split; checked rows vs the oracle."""
+    idx = torch.as_tensor(rows_checked, device=t.device)
+    x = to_host_f64(t[idx])
+    api.rdfft_forward(t)
+    torch.cuda.synchronize()
+    assert_close(to_host_f64(t[idx]), ord_.rdfft_forward(x), dtype, f"{what} forward")
+    y = to_host_f64(t[idx])
+    api.rdfft_inverse(t)
+    torch.cuda.synchronize()
+    assert_close(to_host_f64(t[idx]), ord_.rdfft_inverse(y), dtype, f"{what} inverse")
+
+
+def test_launch_split_beyond_grid_limit_n2():
+    """2^31 + 3 rows of n = 2 (8 GiB of bf16): more rows than one launch's grid holds."""
+    rows = (1 << 31) + 3
+    t = torch.ones((rows, 2), dtype=torch.bfloat16, device="cuda")
+    edge = [0, 1, (1 << 31) - 2, (1 << 31) - 1, 1 << 31, (1 << 31) + 1, rows - 1]
+    vals = inputs.normal_rows(4321, len(edge), 2, "bf16")
+    t[torch.as_tensor(edge, device="cuda")] = to_device(vals, "bf16")
+    _split_rows_check(t, 2, "bf16", edge, "split n=2")
+    # every other row was (1, 1): forward gives (2, 0), the inverse brings it back exactly
+    t[torch.as_tensor(edge, device="cuda")] = 1
+    for r0 in range(0, rows, 1 << 28):
+        assert bool((t[r0 : r0 + (1 << 28)] == 1).all()), r0
+    del t
+    torch.cuda.empty_cache()
+
+
+def test_launch_split_beyond_grid_limit_mixed():
+    """Mixed-radix rows: 2^25 + 7 rows of n = 6 exceed one launch of 64-thread workgroups."""
+    rows = (1 << 25) + 7
+    t = torch.ones((rows, 6), dtype=torch.float32, device="cuda")
+    edge = [0, (1 << 25) - 1, 1 << 25, rows - 1]
+    t[torch.as_tensor(edge, device="cuda")] = to_device(inputs.normal_rows(4322, len(edge), 6, "f32"), "f32")
+    _split_rows_check(t, 6, "f32", edge, "split n=6")
+    t[torch.as_tensor(edge, device="cuda")] = 1
+    assert float((t - 1).abs().max()) < 1e-6
+    del t
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("n", [128, 4096, 65536])
 def test_bitwise_deterministic(n):
     x = inputs.normal_rows(_seed(n, "f32", 5), _rows_for(n), n, "f32")
