@@ -5,8 +5,10 @@
 // live in the caller's own output buffers, so the layer still needs no memory beyond
 // them:
 //   forward   X_tj = FFT(x_tj) into y's segment j (needs kb <= q), then per bin
-//             Y_ti = sum_j C_ij X_tj in place, then y_ti = IFFT(Y_ti) in place.  With
-//             q == kb == 1 the product is applied as the inverse transform loads.
+//             Y_ti = sum_j C_ij X_tj in place, then y_ti = IFFT(Y_ti) in place.  A single
+//             circulant (q == kb == 1) instead runs both transforms and the product in
+//             one row kernel, the spectrum staying in registers (p <= 32768), or takes
+//             the product as the inverse loads (p = 65536).
 //   backward  G_ti = FFT(g_ti) in place in gy; X_tj = FFT(x_tj) into dx; per bin
 //             dC_ij = sum_t conj(X_tj) G_ti (float32 atomics into dc); per bin
 //             dX_tj = sum_i conj(C_ij) G_ti into dx; dx_tj = IFFT(dX_tj) in place; the
@@ -118,6 +120,59 @@ __global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
                                                               typename S::Const{spec}};
   const typename S::Acc out{dst + row * (int64_t)P::N};
   row_inverse<LOGN, false, decltype(in), typename S::Acc, CH>(t, true, in, out, lds, tw);
+}
+
+// y row r = IFFT(spec . FFT(x row r)) for one block spectrum spec (a single circulant,
+// q == kb == 1): the forward post-pass leaves thread t the slots the inverse pre-pass of
+// the same thread reads (RegSpectrum), so the row goes from x to y in one pass over HBM.
+// Every load of a row precedes its first store, so x may be y.
+template <int LOGN, class Elem>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
+    mp_circulant_kernel(const Elem* x, Elem* y, const Elem* spec, int64_t rows, const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, Elem>();
+  using P = RowPlan<LOGN, CH>;
+  static_assert(P::RW == 1, "one row per workgroup");
+  constexpr int N = P::N, E = P::E, TPR = P::TPR;
+  constexpr int R0 = radix(LOGN, 0), BPT0 = E / R0;
+  using S = StorageOf<Elem>;
+  __shared__ float2 lds[P::LDS_F2];
+  const int t = threadIdx.x;
+  const int64_t row = blockIdx.x;
+  if (row >= rows) return;
+  typename S::Const::raw_t raw[E];
+  load_forward<LOGN>(t, typename S::Const{x + row * (int64_t)N}, raw);
+  float2 lo[E / 2], hi[E / 2];
+  // DST_IN_LDS: a barrier after the post-pass's last LDS read, before the inverse's writes
+  row_forward_loaded<LOGN, true, typename S::Const, RegSpectrum, CH>(t, true, raw, RegSpectrum{lo, hi}, lds, tw);
+  // Y . C on slot k_j = t + j*TPR and its partner; slot 0 (thread 0, j = 0) holds the two
+  // real bins Y_0, Y_{n/2}, and its partner is the complex bin N/2
+  const typename S::Const cin{spec};
+  static_for<E / 2>([&](auto jc) {
+    constexpr int j = decltype(jc)::value;
+    const int k = t + j * TPR;
+    if constexpr (j == 0) {
+      const bool z = t == 0;
+      const float2 c0 = cin.load(k), ch = cin.load(z ? N / 2 : N - k);
+      lo[0] = z ? make_float2(lo[0].x * c0.x, lo[0].y * c0.y) : c_mul<false>(lo[0], c0);
+      hi[0] = c_mul<false>(hi[0], ch);
+    } else {
+      lo[j] = c_mul<false>(lo[j], cin.load(k));
+      hi[j] = c_mul<false>(hi[j], cin.load(N - k));
+    }
+  });
+  // the inverse reads slot m = t + TPR*(b + BPT0*r) at raw[b*R0 + r], its partner at
+  // raw[b*R0 + R0/2 + r]
+  float2 inv[E];
+  static_for<BPT0>([&](auto bc) {
+    constexpr int b = decltype(bc)::value;
+    static_for<R0 / 2>([&](auto rc) {
+      constexpr int r = decltype(rc)::value;
+      inv[b * R0 + r] = lo[b + BPT0 * r];
+      inv[b * R0 + R0 / 2 + r] = hi[b + BPT0 * r];
+    });
+  });
+  row_inverse_loaded<LOGN, false, RegSource, typename S::Acc, CH>(t, true, inv, typename S::Acc{y + row * (int64_t)N},
+                                                                  lds, tw);
 }
 
 // Per bin, in place in y: Y_ti = sum_j C_ij X_tj, with X_tj in y's segment j (kb <= q).
@@ -240,10 +295,33 @@ hipError_t per_row_slots(int64_t nrows, int per, F launch) {
 }
 
 template <int LOGN, class Elem>
+hipError_t circulant_rows(const void* x, void* y, const void* spec, int64_t rows, const float2* tw,
+                          hipStream_t stream) {
+  constexpr int N = 1 << LOGN;
+  using P = RowPlan<LOGN, mp_chunks<LOGN, Elem>()>;
+  for (int64_t r0 = 0; r0 < rows;) {
+    const int64_t nr = std::min<int64_t>(rows - r0, kMaxGridThreads / P::WG);
+    hipLaunchKernelGGL((mp_circulant_kernel<LOGN, Elem>), dim3((unsigned)nr), dim3(P::WG), 0, stream,
+                       static_cast<const Elem*>(x) + r0 * (int64_t)N, static_cast<Elem*>(y) + r0 * (int64_t)N,
+                       static_cast<const Elem*>(spec), nr, tw);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    r0 += nr;
+  }
+  return hipSuccess;
+}
+
+template <int LOGN, class Elem>
 hipError_t mp_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
   constexpr int N = 1 << LOGN;
   const int storage = StorageOf<Elem>::kHalf ? kStorageBF16 : kStorageF32;
   const int64_t xrows = a.tokens * a.kb;
+  // single circulant: one fused row pass where the registers hold both spectra (p <= 32768);
+  // for p = 65536 the row already fills the registers, so forward, then inverse with the
+  // product taken as it loads
+  if constexpr (LOGN < kMpMaxLogN) {
+    if (a.q == 1 && a.kb == 1) return circulant_rows<LOGN, Elem>(a.x, a.y, a.c, xrows, tw, stream);
+  }
   hipError_t e = forward_rows<LOGN, Elem>(a.x, a.y, xrows, a.kb, a.q, tw, stream);
   if (e != hipSuccess) return e;
   if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, Elem, false>(a.y, a.y, a.c, xrows, tw, stream);

@@ -244,6 +244,20 @@ struct LdsSpectrum {
   __device__ __forceinline__ void store(int m, float2 v) const { base[lds_pad(m)] = v; }
 };
 
+// A packed spectrum kept in the caller's registers.  The forward post-pass of thread t
+// produces the pair slots k_j = t + j*TPR, j < E/2, and their partners N - k_j (N/2 for
+// k_j == 0); these are exactly the slots the inverse pre-pass of the same thread reads
+// (load_inverse), so a row can pass from one transform to the other without an exchange.
+struct RegSpectrum {
+  float2* lo;  // [E/2]: slot k_j
+  float2* hi;  // [E/2]: slot N - k_j, or N/2 for k_j == 0
+};
+// Its counterpart as a source: raw values already in float32
+struct RegSource {
+  using raw_t = float2;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return r; }
+};
+
 // lds_pad(base + j*stride) == lds_pad(base) + pad_step(j*stride) whenever the low four
 // bits of base plus those of j*stride stay below 16.  Every Stockham exchange address has
 // that form (base's low bits are below the sub-transform stride, or the stride is a
@@ -494,8 +508,14 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
           hi = z ? zh : hi;
           hi_idx = z ? N / 2 : hi_idx;
         }
-        dst.store(k, lo);
-        dst.store(hi_idx, hi);
+        if constexpr (std::is_same<Dst, RegSpectrum>::value) {
+          // k = t + TPR*(b + BPL*r): register index j = b + BPL*r
+          dst.lo[b + BPL * r] = lo;
+          dst.hi[b + BPL * r] = hi;
+        } else {
+          dst.store(k, lo);
+          dst.store(hi_idx, hi);
+        }
       });
     });
   }

@@ -130,6 +130,8 @@ LONG = [
     (3, 65536, 65536, 65536, "f32"),
     (2, 65536, 65536, 65536, "bf16"),
     (37, 16384, 32768, 16384, "bf16"),  # q = 2, kb = 1, more tokens than dC chunks
+    (6, 32768, 32768, 32768, "bf16"),  # single circulants: the fused row kernel
+    (4, 32768, 32768, 32768, "f32"),
 ]
 
 
@@ -163,10 +165,12 @@ def test_long_blocks(shape):
     _check(x, c, g, dtype, d_out, p, got, str(shape), sampled=3)
 
 
+@pytest.mark.parametrize("d", [16384, 32768])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_long_blocks_in_place_forward(dtype):
-    """y may be x for long blocks too; dx must then be its own buffer (not gy)."""
-    tokens, d, p = 3, 32768, 16384
+def test_long_blocks_in_place_forward(dtype, d):
+    """y may be x for long blocks too (a single circulant, and 2 x 2 blocks); dx must then
+    be its own buffer (not gy)."""
+    tokens, p = 3, 16384
     x, c, g = _problem(77, tokens, d, d, p, 0.004, dtype)
     got = _run(x, c, g, dtype, d, alias_y=True)
     _check(x, c, g, dtype, d, p, got, "long aliased y")
