@@ -789,6 +789,7 @@ hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t st
       {sq_fwd_table<1>(true, seq), sq_fwd_table<2>(true, seq), sq_fwd_table<3>(true, seq),
        sq_fwd_table<4>(true, seq)}};
   if (a.logp - 1 > kBcaMaxLogN) return launch_bca_multipass(a, false, tw, stream, num_cu);
+  if (a.logp - 1 == kCirculantLogN && a.q == 1 && a.kb == 1) return launch_bca_circulant(a, tw, stream);
   if (a.q == a.kb && a.q <= kSqMaxBlocks) {
     const BcaBwdFn fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
     if (fn != nullptr) return fn(a, tw, stream, num_cu);

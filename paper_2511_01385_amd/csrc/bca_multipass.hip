@@ -387,6 +387,12 @@ bool bca_multipass_supported(int logp, int q, int kb, bool backward) {
   return kb <= q && kb <= kMpMaxKb;
 }
 
+hipError_t launch_bca_circulant(const BcaArgs& a, const float2* tw, hipStream_t stream) {
+  if (a.logp - 1 != kCirculantLogN || a.q != 1 || a.kb != 1) return hipErrorInvalidValue;
+  return a.bf16 ? circulant_rows<kCirculantLogN, uint32_t>(a.x, a.y, a.c, a.tokens, tw, stream)
+                : circulant_rows<kCirculantLogN, float2>(a.x, a.y, a.c, a.tokens, tw, stream);
+}
+
 hipError_t launch_bca_multipass(const BcaArgs& a, bool backward, const float2* tw, hipStream_t stream, int num_cu) {
   static const auto seq = std::make_integer_sequence<int, kMpMaxLogN - kMpMinLogN + 1>{};
   static const std::array<MpFn, kMpMaxLogN - kMpMinLogN + 1> tab[2][2] = {

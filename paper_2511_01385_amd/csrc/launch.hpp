@@ -61,6 +61,11 @@ bool bca_shape_supported(int logp, int q, int kb, bool backward);
 // (the input spectra are staged in dx while gy holds the upstream spectra).  The
 // backward launcher expects dc zeroed and leaves it as packed spectra.
 bool bca_multipass_supported(int logp, int q, int kb, bool backward);
+// The forward of a single circulant (q == kb == 1) of p = 2^(kCirculantLogN+1) = 8192 as
+// one row kernel per token (bca_multipass.hip), the spectrum handed from the forward to
+// the inverse transform in registers.
+constexpr int kCirculantLogN = 12;
+hipError_t launch_bca_circulant(const BcaArgs& a, const float2* tw, hipStream_t stream);
 hipError_t launch_bca_multipass(const BcaArgs& a, bool backward, const float2* tw, hipStream_t stream, int num_cu);
 
 }  // namespace rdfft
