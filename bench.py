@@ -18,9 +18,10 @@ the dominant kernel; inside the timed steps only that call is bracketed by HIP e
 (on its launch stream), and its algorithmic bytes over its average event-timed
 duration give `achieved`.  per_call_probe lists every call from the probe steps.  per_config (after the timed steps,
 outside `value`) times every workload shape of the paper's configurations on its own:
-fp32 and bf16 transforms for each n, n = 65536 fp32, and the three layer shapes.
+fp32 and bf16 transforms for each n, n = 65536 fp32, two mixed-radix lengths, the three
+layer shapes and one 65536-wide circulant.
 
-Prints one JSON line.  --gpus above 1 is refused: this build runs on one GPU.
+Prints one JSON line.  --gpus above 1 is refused: the benchmark measures one GPU.
 """
 
 from __future__ import annotations
@@ -226,8 +227,9 @@ def copy_rate(dev, stream, reps: int = 5):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py: --gpus {args.gpus} requested, but this build measures one GPU only "
-              "(rows and tokens would shard across GPUs with one dc all-reduce; see DESIGN.md)", file=sys.stderr)
+        print(f"bench.py: --gpus {args.gpus} requested, but the benchmark measures one GPU only "
+              "(rows and tokens would shard across GPUs with one all-reduce of dc, which is not implemented)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch

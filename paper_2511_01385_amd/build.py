@@ -24,7 +24,9 @@ SOURCES = ["rdfft_kernels.hip", "bca_kernels.hip", "bca_multipass.hip", "layout_
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
-# Packed FP32 instructions are disabled for every HIP object.
+# Packed FP32 instructions (v_pk_*_f32) are disabled for every HIP object: the compiler
+# would otherwise form them from float2 arithmetic, and the kernels are written for the
+# scalar FP32 forms.
 COMMON = [
     "-O3",
     "-std=c++17",
