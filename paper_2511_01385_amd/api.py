@@ -39,6 +39,9 @@ def _dev(t: torch.Tensor, name: str) -> int:
 
 
 def _stream(t: torch.Tensor) -> int:
+    if t.device.index is not None and t.device.index != torch.cuda.current_device():
+        # the library works on the current device
+        raise ValueError(f"tensor on {t.device}, current device is cuda:{torch.cuda.current_device()}")
     return torch.cuda.current_stream(t.device).cuda_stream
 
 
@@ -81,10 +84,31 @@ def rdfft_halfcomplex_to_pairs(buf: torch.Tensor) -> torch.Tensor:
     return buf
 
 
+def _layer_shapes(x: torch.Tensor, c_spectra: torch.Tensor, out: torch.Tensor, out_name: str):
+    """(q, kb, p, tokens) after checking that the tensors agree with each other.
+
+    The library sees only pointers and sizes, so a tensor of the wrong shape, storage type
+    or device would make it read or write outside that tensor; those are refused here.
+    """
+    if c_spectra.dim() != 3:
+        raise ValueError(f"c_spectra must have shape (q, kb, p), got {tuple(c_spectra.shape)}")
+    q, kb, p = c_spectra.shape
+    if x.dim() != 2 or x.shape[1] != kb * p:
+        raise ValueError(f"x must have shape (tokens, {kb * p}), got {tuple(x.shape)}")
+    tokens = x.shape[0]
+    if tuple(out.shape) != (tokens, q * p):
+        raise ValueError(f"{out_name} must have shape ({tokens}, {q * p}), got {tuple(out.shape)}")
+    for name, t in (("c_spectra", c_spectra), (out_name, out)):
+        if t.dtype != x.dtype:
+            raise TypeError(f"{name} is {t.dtype}, x is {x.dtype}")
+        if t.device != x.device:
+            raise ValueError(f"{name} is on {t.device}, x on {x.device}")
+    return q, kb, p, tokens
+
+
 def bca_forward(x: torch.Tensor, c_spectra: torch.Tensor, y: torch.Tensor) -> torch.Tensor:
     """y[t] = W x[t] for the block-circulant W whose packed block spectra are ``c_spectra`` (q, kb, p)."""
-    q, kb, p = c_spectra.shape
-    tokens = x.shape[0]
+    q, kb, p, tokens = _layer_shapes(x, c_spectra, y, "y")
     st = _lib.load().bca_forward(
         _dev(x, "x"), _dev(c_spectra, "c_spectra"), _dev(y, "y"), None,
         kb * p, q * p, p, tokens, _code(x), _stream(x),
@@ -99,8 +123,11 @@ def bca_backward(x: torch.Tensor, c_spectra: torch.Tensor, gy: torch.Tensor, dx:
     ``gy`` is left unspecified; ``dx`` may be ``gy`` itself when d_in == d_out and p <= 8192
     (longer blocks stage the input spectra in ``dx``).
     """
-    q, kb, p = c_spectra.shape
-    tokens = x.shape[0]
+    q, kb, p, tokens = _layer_shapes(x, c_spectra, gy, "gy")
+    if tuple(dx.shape) != tuple(x.shape) or dx.dtype != x.dtype or dx.device != x.device:
+        raise ValueError(f"dx must match x: {tuple(x.shape)} {x.dtype} on {x.device}")
+    if tuple(dc.shape) != (q, kb, p) or dc.device != x.device:
+        raise ValueError(f"dc must have shape ({q}, {kb}, {p}) on {x.device}, got {tuple(dc.shape)}")
     if dc.dtype != torch.float32:
         raise TypeError("dc is float32")
     grads = _lib.BcaGrads(_dev(dx, "dx"), _dev(dc, "dc"))
