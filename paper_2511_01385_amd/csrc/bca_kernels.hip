@@ -397,6 +397,7 @@ template <int LOGN, class Elem, int QB, int WG = BcaPlan<LOGN>::BWD_WG>
 __global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
                                                                       const Elem* gy, Elem* dx, float* __restrict__ dc,
                                                                       int64_t tokens, int tt_per_tile, int64_t ntiles,
+                                                                      float2* stage, int64_t tile_f2, int chunk,
                                                                       const float2* __restrict__ tw) {
   using B = BcaPlan<LOGN>;
   using S = BcaSq<LOGN, QB, WG>;
@@ -508,6 +509,19 @@ __global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const Elem* __restr
     });
   });
   __syncthreads();
+  if (stage != nullptr) {
+    // Two-stage sum (dx is not gy): the partial sums go to the gy rows of this workgroup's
+    // first tiles, which it alone has read and nobody reads again, chunk c of them (chunk
+    // float2 each) to tile blockIdx.x + c*gridDim.x; bca_dc_reduce_kernel then adds the
+    // workgroups' partials into dc.
+    for (int e = tid; e < QKN; e += WG) {
+      float2 v = part[e];
+      static_for<TS - 1>([&](auto pc) { v = c_add(v, part[(size_t)(decltype(pc)::value + 1) * QKN + e]); });
+      const int ch = e / chunk;
+      stage[((int64_t)blockIdx.x + (int64_t)ch * gridDim.x) * tile_f2 + (e - ch * chunk)] = v;
+    }
+    return;
+  }
   const int shift = (int)(((unsigned)blockIdx.x * 64u) % (unsigned)QKN);
   for (int e0 = tid; e0 < QKN; e0 += WG) {
     int e = e0 + shift;
@@ -517,6 +531,27 @@ __global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const Elem* __restr
     unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
     unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
   }
+}
+
+// Second stage of the two-stage dC sum: dc[e] += the partials of workgroups
+// b in [blockIdx.y*kReduceGroup, +kReduceGroup) (zeroed dc, one float32 atomic pair per
+// thread and group of workgroups).  Workgroup b's slot e lies at
+// stage[(b + c*groups)*tile_f2 + e - c*chunk], c = e / chunk.
+constexpr int kReduceGroup = 16;
+constexpr int64_t kStageMinAtomics = (int64_t)1 << 21;
+__global__ void __launch_bounds__(256) bca_dc_reduce_kernel(const float2* __restrict__ stage, float* __restrict__ dc,
+                                                            int qkn, int chunk, int groups, int64_t tile_f2) {
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= qkn) return;
+  const int ch = e / chunk;
+  const int b0 = blockIdx.y * kReduceGroup;
+  const int b1 = b0 + kReduceGroup < groups ? b0 + kReduceGroup : groups;
+  const float2* p = stage + ((int64_t)ch * groups + b0) * tile_f2 + (e - ch * chunk);
+  float2 v = make_float2(0.f, 0.f);
+#pragma unroll 8
+  for (int b = b0; b < b1; ++b, p += tile_f2) v = c_add(v, *p);
+  unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
+  unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
 }
 
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
@@ -729,9 +764,25 @@ static hipError_t bwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t st
   const int64_t tiles = (a.tokens + TT - 1) / TT;
   const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / WG));
   const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
+  // Two-stage dC sum when dx has its own buffer: each workgroup's partial sums (QKN float2)
+  // fit in the gy rows of its first `chunks` tiles, all of them full tiles
+  constexpr int QKN = QB * QB * S::N;
+  const int64_t tile_bytes = (int64_t)TT * QB * S::N * (int64_t)sizeof(Elem);
+  const int64_t tile_f2 = tile_bytes / (int64_t)sizeof(float2);
+  const int chunk = (int)std::max<int64_t>(1, std::min<int64_t>(QKN, tile_f2));
+  const int64_t chunks = (QKN + chunk - 1) / chunk;
+  // (worth a second launch only when the atomics it replaces are many: 4.2M float32 atomics
+  // for the 4096-wide layer took ~24 us, 0.6M for the 768-wide one less than the launch)
+  const bool staged = a.dx != a.y && tile_bytes % (int64_t)sizeof(float2) == 0 && chunks * grid <= a.tokens / TT &&
+                      2 * (int64_t)QKN * grid >= kStageMinAtomics;
+  float2* const stage = staged ? static_cast<float2*>(a.y) : nullptr;
   hipLaunchKernelGGL((bca_backward_sq_kernel<LOGN, Elem, QB>), dim3((unsigned)grid), dim3(WG), lds, stream,
                      static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<const Elem*>(a.y),
-                     static_cast<Elem*>(a.dx), a.dc, a.tokens, TT, tiles, tw);
+                     static_cast<Elem*>(a.dx), a.dc, a.tokens, TT, tiles, stage, tile_f2, chunk, tw);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || !staged) return e;
+  const dim3 rgrid((unsigned)((QKN + 255) / 256), (unsigned)((grid + kReduceGroup - 1) / kReduceGroup));
+  hipLaunchKernelGGL(bca_dc_reduce_kernel, rgrid, dim3(256), 0, stream, stage, a.dc, QKN, chunk, (int)grid, tile_f2);
   return hipGetLastError();
 }
 

@@ -180,6 +180,20 @@ def test_long_blocks_in_place_forward(dtype, d):
         api.bca_backward(xt, ct, gt, gt, dct)
 
 
+# square layers with enough tokens for the two-stage dC sum (dx apart from gy); 2048 bf16
+# tokens fill exactly the tiles it needs; with dx == gy the same shapes take the atomics
+STAGED = [(4096, 4096, 1024, "f32", False), (2048, 4096, 1024, "bf16", False), (4096, 4096, 1024, "bf16", True)]
+
+
+@pytest.mark.parametrize("shape", STAGED, ids=[f"T{s[0]}_{s[1]}_p{s[2]}_{s[3]}_{'aliased' if s[4] else 'apart'}"
+                                               for s in STAGED])
+def test_square_layer_dc_sums(shape):
+    tokens, d, p, dtype, alias = shape
+    x, c, g = _problem(606 + tokens, tokens, d, d, p, 0.01, dtype)
+    got = _run(x, c, g, dtype, d, alias_dx=alias)
+    _check(x, c, g, dtype, d, p, got, str(shape))
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_in_place_layer(dtype):
     """y may be x itself, and dx may be gy itself, when d_in == d_out."""
