@@ -181,8 +181,10 @@ def test_long_blocks_in_place_forward(dtype, d):
 
 
 # square layers with enough tokens for the two-stage dC sum (dx apart from gy); 2048 bf16
-# tokens fill exactly the tiles it needs; with dx == gy the same shapes take the atomics
-STAGED = [(4096, 4096, 1024, "f32", False), (2048, 4096, 1024, "bf16", False), (4096, 4096, 1024, "bf16", True)]
+# tokens fill exactly the tiles it needs, 4093 leave a partial last tile; with dx == gy the
+# same shapes take the atomics
+STAGED = [(4096, 4096, 1024, "f32", False), (2048, 4096, 1024, "bf16", False), (4093, 4096, 1024, "bf16", False),
+          (4096, 4096, 1024, "bf16", True)]
 
 
 @pytest.mark.parametrize("shape", STAGED, ids=[f"T{s[0]}_{s[1]}_p{s[2]}_{s[3]}_{'aliased' if s[4] else 'apart'}"
