@@ -18,7 +18,7 @@ the dominant kernel; inside the timed steps only that call is bracketed by HIP e
 (on its launch stream), and its algorithmic bytes over its average event-timed
 duration give `achieved`.  per_call_probe lists every call from the probe steps.  per_config (after the timed steps,
 outside `value`) times every workload shape of the paper's configurations on its own:
-fp32 and bf16 transforms for each n, n = 65536 fp32, two mixed-radix lengths, the three
+fp32 and bf16 transforms for each n, n = 65536 fp32, two mixed-radix lengths, the four
 layer shapes and one 65536-wide circulant.
 
 Prints one JSON line.  --gpus above 1 is refused: the benchmark measures one GPU.
@@ -132,9 +132,9 @@ def config_table(dev, stream, reps: int = 10):
     Batched transforms for each n in 64..4096 (2^16 rows) in fp32 and bf16 storage,
     n = 65536 (1024 rows, fp32) and the mixed-radix lengths n = 3000 (fp32) and n = 6144
     (bf16, 2^16 rows each), forward and inverse, each over a rotating >= 1 GiB pool;
-    and the three layer shapes (768-wide p = 256, 4096-wide p = 1024, 8192-wide p = 8192,
-    bf16, 4096 tokens) and one 65536-wide circulant (p = 65536, bf16, 1024 tokens; the
-    multi-pass layer) forward and backward.  GB/s are algorithmic bytes over the
+    and the four layer shapes (256-wide p = 64, fp32, 128 tokens; 768-wide p = 256,
+    4096-wide p = 1024, 8192-wide p = 8192, bf16, 4096 tokens) and one 65536-wide circulant
+    (p = 65536, bf16, 1024 tokens; the multi-pass layer) forward and backward.  GB/s are algorithmic bytes over the
     event-timed average of `reps` back-to-back calls; frac is of 8 TB/s.
     """
     import torch
@@ -184,21 +184,24 @@ def config_table(dev, stream, reps: int = 10):
             "frac": round((gbs_f + gbs_i) / 2 / HBM_PEAK_GBS, 4)}
         del pool
     torch.cuda.empty_cache()
-    # the paper's three layer shapes, then one circulant beyond the fused kernels' blocks
-    for d, p, T in ((768, 256, 4096), (4096, 1024, 4096), (8192, 8192, 4096), (65536, 65536, 1024)):
+    # the paper's four layer shapes (the 256-wide one in fp32), then one circulant beyond the
+    # fused kernels' blocks
+    for d, p, T, dt in ((256, 64, 128, "f32"), (768, 256, 4096, "bf16"), (4096, 1024, 4096, "bf16"),
+                        (8192, 8192, 4096, "bf16"), (65536, 65536, 1024, "bf16")):
         q = kb = d // p
-        nset = max(2, -(-POOL_BYTES // (4 * T * d * 2)))
-        sets = [dict(x=torch.randn(T, d, device=dev).to(torch.bfloat16),
-                     c=(0.02 * torch.randn(q, kb, p, device=dev)).to(torch.bfloat16),
-                     g=torch.randn(T, d, device=dev).to(torch.bfloat16),
-                     y=torch.empty(T, d, device=dev, dtype=torch.bfloat16),
-                     dx=torch.empty(T, d, device=dev, dtype=torch.bfloat16),
+        tdt, s = (torch.float32, 4) if dt == "f32" else (torch.bfloat16, 2)
+        nset = max(2, -(-POOL_BYTES // (4 * T * d * s)))
+        sets = [dict(x=torch.randn(T, d, device=dev).to(tdt),
+                     c=(0.02 * torch.randn(q, kb, p, device=dev)).to(tdt),
+                     g=torch.randn(T, d, device=dev).to(tdt),
+                     y=torch.empty(T, d, device=dev, dtype=tdt),
+                     dx=torch.empty(T, d, device=dev, dtype=tdt),
                      dc=torch.empty(q, kb, p, device=dev)) for _ in range(nset)]
         us_f = timed(lambda st: api.bca_forward(st["x"], st["c"], st["y"]), [(st,) for st in sets])
         us_b = timed(lambda st: api.bca_backward(st["x"], st["c"], st["g"], st["dx"], st["dc"]), [(st,) for st in sets])
-        bf = 2 * T * d * 2 + q * kb * p * 2
-        bb = 3 * T * d * 2 + q * kb * p * 2 + q * kb * p * 4
-        table[f"bca_bf16_d{d}_p{p}_T{T}"] = {
+        bf = 2 * T * d * s + q * kb * p * s
+        bb = 3 * T * d * s + q * kb * p * s + q * kb * p * 4
+        table[f"bca_{dt}_d{d}_p{p}_T{T}"] = {
             "forward_us": round(us_f, 2), "backward_us": round(us_b, 2),
             "forward_GB_s": round(bf / us_f / 1e3, 1), "backward_GB_s": round(bb / us_b / 1e3, 1)}
         del sets
