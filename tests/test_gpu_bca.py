@@ -225,8 +225,9 @@ def test_dc_overwritten_not_accumulated():
     np.testing.assert_allclose(a, b, rtol=1e-6, atol=1e-6 * np.abs(a).max())
 
 
-def test_no_device_allocation():
-    tokens, d, p = 512, 4096, 1024
+@pytest.mark.parametrize("tokens,d,p", [(512, 4096, 1024), (4096, 4096, 1024), (64, 16384, 16384), (64, 32768, 16384)],
+                         ids=["atomic_dc", "two_stage_dc", "circulant_16384", "long_blocks_2x2"])
+def test_no_device_allocation(tokens, d, p):
     x, c, g = _problem(7, tokens, d, d, p, 0.01, "bf16")
     xt, ct, gt = to_device(x, "bf16"), to_device(c, "bf16"), to_device(g, "bf16")
     yt = torch.empty_like(xt)

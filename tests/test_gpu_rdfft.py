@@ -279,8 +279,9 @@ def test_special_inputs_closed_forms():
     np.testing.assert_allclose(got, want, atol=2e-3)
 
 
-def test_no_device_allocation():
-    x = to_device(inputs.normal_rows(9, 4096, 1024, "bf16"), "bf16")
+@pytest.mark.parametrize("n", [1024, 3000])
+def test_no_device_allocation(n):
+    x = to_device(inputs.normal_rows(9, 4096, n, "bf16"), "bf16")
     api.rdfft_forward(x)  # first use on this device: table upload
     torch.cuda.synchronize()
     alloc0 = torch.cuda.memory_allocated()
