@@ -9,10 +9,13 @@
 // so no intermediate tensor ever reaches HBM.  Slot 0 of a packed spectrum holds
 // the two real bins Y_0 and Y_{p/2}; every product acts on them as two real
 // products (conjugation is the identity there).  The backward runs one wide persistent
-// workgroup per CU; its dC partial sums stay in LDS for all of its tiles and are then
-// added into the caller's dc buffer with float32 atomics (each workgroup starting at a
-// different offset); a final in-place irdFFT of dc (stream-ordered after the kernel)
-// yields the time-domain gradient.
+// workgroup per CU; its dC partial sums stay in LDS (or registers) for all of its tiles
+// and are then added into the caller's dc buffer with float32 atomics (each workgroup
+// starting at a different offset), or, for the square-layer kernel when dx is not gy,
+// staged in the gy rows the workgroup has consumed and summed by a second kernel; a final
+// in-place irdFFT of dc (stream-ordered after the kernels) yields the time-domain
+// gradient.  A single circulant of p = 8192 and blocks beyond 8192 are routed to the row
+// kernels of bca_multipass.hip.
 #include <hip/hip_runtime.h>
 
 #include "fft_device.hpp"
