@@ -30,6 +30,7 @@ import argparse
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -62,13 +63,19 @@ def parse():
 
 
 def source_digest() -> str:
-    """Digest of the kernel sources, to tell whether stored counter readings are current."""
+    """Digest of the kernel sources, to tell whether stored counter readings are current.
+
+    Comments and blank lines are left out (the sources hold no string literal with "//" or
+    "/*"), so an edit of a comment does not invalidate the readings; any code edit does.
+    """
     h = hashlib.sha256()
     csrc = os.path.join(ROOT, "paper_2511_01385_amd", "csrc")
     for name in sorted(os.listdir(csrc)):
         if name.endswith((".hip", ".hpp", ".cpp", ".h")):
-            with open(os.path.join(csrc, name), "rb") as f:
-                h.update(name.encode() + f.read())
+            with open(os.path.join(csrc, name), encoding="utf-8") as f:
+                text = re.sub(r"/\*.*?\*/", "", f.read(), flags=re.S)
+            code = [line.split("//", 1)[0].rstrip() for line in text.splitlines()]
+            h.update(name.encode() + "\n".join(line for line in code if line).encode())
     return h.hexdigest()[:16]
 
 
