@@ -32,7 +32,7 @@ constexpr int kPlan[kMaxLogN + 1][5] = {
     {16, 16, 16},     // 4096
     {16, 16, 8, 4},   // 8192
     {16, 16, 16, 4},  // 16384
-    {16, 16, 16, 8},  // 32768
+    {32, 32, 32},     // 32768
 };
 
 // Complex values each thread holds (E) and LDS exchange chunks (C).  With C > 1 a
