@@ -419,6 +419,12 @@ __global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const Elem* __restr
   float2* const gs = bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: G
   // spare region for row groups without a transform (allocated only when some exist)
   float2* const dummy = bca_lds + (size_t)TT * 2 * QB * REG;
+  if (stage != nullptr) {
+    // two-stage sum: this kernel never touches dc, and the reduce kernel that adds into it
+    // runs after it on the stream, so dc is zeroed here instead of by a launch of its own
+    for (int64_t e = (int64_t)blockIdx.x * WG + tid; e < 2 * (int64_t)QB * QB * N; e += (int64_t)gridDim.x * WG)
+      dc[e] = 0.f;
+  }
 
   // slot (i, jj) is sl = i*JPT + jj, for input block j = j0 + jj.  C is kept in its
   // storage form (half the registers for bf16) and widened where it is used.
@@ -560,6 +566,12 @@ __global__ void __launch_bounds__(256) bca_dc_reduce_kernel(const float2* __rest
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += (int64_t)gridDim.x * blockDim.x)
     p[i] = 0.f;
+}
+
+static hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t stream) {
+  const int blocks = (int)std::min<int64_t>((count + 255) / 256, 1024);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, p, count);
+  return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------------
@@ -779,6 +791,10 @@ static hipError_t bwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t st
   const bool staged = a.dx != a.y && tile_bytes % (int64_t)sizeof(float2) == 0 && chunks * grid <= a.tokens / TT &&
                       2 * (int64_t)QKN * grid >= kStageMinAtomics;
   float2* const stage = staged ? static_cast<float2*>(a.y) : nullptr;
+  if (!staged) {  // the kernel's atomics add into dc
+    const hipError_t ez = launch_fill_zero(a.dc, 2 * (int64_t)QKN, stream);
+    if (ez != hipSuccess) return ez;
+  }
   hipLaunchKernelGGL((bca_backward_sq_kernel<LOGN, Elem, QB>), dim3((unsigned)grid), dim3(WG), lds, stream,
                      static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<const Elem*>(a.y),
                      static_cast<Elem*>(a.dx), a.dc, a.tokens, TT, tiles, stage, tile_f2, chunk, tw);
@@ -855,20 +871,25 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
   static const auto seq = std::make_integer_sequence<int, kBcaMaxLogN + 1>{};
   static const std::array<BcaBwdFn, kBcaMaxLogN + 1> tab[2] = {bwd_table(false, seq), bwd_table(true, seq)};
   const int64_t slots = (int64_t)a.q * a.kb * ((int64_t)1 << (a.logp - 1)) * 2;
-  const int blocks = (int)std::min<int64_t>((slots + 255) / 256, 1024);
-  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, a.dc, slots);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.tokens == 0) return e;
   static const std::array<BcaBwdFn, kBcaMaxLogN + 1> sq[2][kSqMaxBlocks] = {
       {sq_table<1>(false, seq), sq_table<2>(false, seq), sq_table<3>(false, seq), sq_table<4>(false, seq)},
       {sq_table<1>(true, seq), sq_table<2>(true, seq), sq_table<3>(true, seq), sq_table<4>(true, seq)}};
-  if (a.logp - 1 > kBcaMaxLogN) {
+  // the square-layer kernels zero dc themselves (in the kernel when the dC sum is staged);
+  // every other path finds it zeroed
+  BcaBwdFn sq_fn = nullptr;
+  if (a.tokens > 0 && a.logp - 1 <= kBcaMaxLogN && a.q == a.kb && a.q <= kSqMaxBlocks)
+    sq_fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
+  hipError_t e = hipSuccess;
+  if (sq_fn == nullptr) {
+    e = launch_fill_zero(a.dc, slots, stream);
+    if (e != hipSuccess || a.tokens == 0) return e;
+  }
+  if (sq_fn != nullptr) {
+    e = sq_fn(a, tw, stream, num_cu);
+  } else if (a.logp - 1 > kBcaMaxLogN) {
     e = launch_bca_multipass(a, true, tw, stream, num_cu);
   } else {
-    BcaBwdFn fn = nullptr;
-    if (a.q == a.kb && a.q <= kSqMaxBlocks) fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
-    if (fn == nullptr) fn = tab[a.bf16 ? 1 : 0][a.logp - 1];
-    e = fn(a, tw, stream, num_cu);
+    e = tab[a.bf16 ? 1 : 0][a.logp - 1](a, tw, stream, num_cu);
   }
   if (e != hipSuccess) return e;
   // dc holds sum_t conj(X) . G as packed spectra; transform them in place to time domain
