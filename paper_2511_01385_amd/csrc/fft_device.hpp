@@ -296,8 +296,40 @@ struct RowPlan {
 
 };
 
+// Mirrored last pass.  When the last pass gives each thread two butterflies and the row
+// has exactly half as many threads as that pass has butterflies (TPR = N/(2 RL)), thread t
+// can take butterflies t and N/RL - t (thread 0: 0 and N/(2 RL)).  Bin k = g + r N/RL of
+// butterfly g and its post-pass partner N - k then sit in the same thread, and the forward
+// post-pass needs no LDS exchange.  Only the standalone row kernels use it: the layer
+// kernels read the spectrum in the plain order.  It costs ~5% more VALU instructions (the
+// selects for thread 0) for one LDS round trip and one barrier fewer: timed, that pays for
+// n >= 2048 (1-2%) and not for n = 64 or 256 (8-12% slower), so shorter rows keep the
+// exchange.
+template <int LOGN>
+constexpr bool mirror_ok() {
+  using P = RowPlan<LOGN>;
+  if constexpr (LOGN < 10 || P::NP < 2) {
+    return false;
+  } else {
+    constexpr int RL = radix(LOGN, P::NP - 1);
+    return P::E / RL == 2 && 2 * P::TPR == P::N / RL && P::TPR > 1;
+  }
+}
+
+// Butterfly of slot b of thread t in pass Q (b a compile-time constant at every call).
+template <int LOGN, int Q, bool MIR>
+__device__ __forceinline__ int bfly(int t, int b) {
+  using P = RowPlan<LOGN>;
+  if constexpr (MIR && Q == P::NP - 1) {
+    constexpr int NsL = P::N / radix(LOGN, Q);
+    return b == 0 ? t : (t == 0 ? NsL / 2 : NsL - t);
+  } else {
+    return t + b * P::TPR;
+  }
+}
+
 // One Stockham pass q: twiddles (q > 0) then radix-R DFTs on the thread's butterflies.
-template <int LOGN, int Q, bool INV>
+template <int LOGN, int Q, bool INV, bool MIR = false>
 __device__ __forceinline__ void stockham_compute(float2* v, int t, const float2* __restrict__ tw) {
   using P = RowPlan<LOGN>;
   constexpr int R = radix(LOGN, Q);
@@ -310,7 +342,7 @@ __device__ __forceinline__ void stockham_compute(float2* v, int t, const float2*
     const float4* __restrict__ twq = reinterpret_cast<const float4*>(tw + kOff);
     static_for<BPT>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
-      const int g = t + b * P::TPR;
+      const int g = bfly<LOGN, Q, MIR>(t, b);
       const int k = g & (Ns - 1);
       // w[r] = W_{Ns*R}^{r*k}: the stored powers r <= L, then w[r] = w[r - L] * w[L]
       float2 w[R > L ? R : L + 1];
@@ -336,7 +368,7 @@ __device__ __forceinline__ void stockham_compute(float2* v, int t, const float2*
 // g writes into chunk g / (N/(R*C)), which is decided by the butterfly slot b when a
 // thread holds at least C butterflies and by the thread index when it holds one; the
 // reads of round c are those with r in chunk c.
-template <int LOGN, int Q, int CH>
+template <int LOGN, int Q, int CH, bool MIR = false>
 __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds) {
   using P = RowPlan<LOGN, CH>;
   constexpr int N = P::N, E = P::E, C = P::C, TPR = P::TPR;
@@ -367,7 +399,7 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
     row_sync<TPR>();
     static_for<BPT2>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
-      const int pg = lds_pad(t + b * TPR);
+      const int pg = lds_pad(bfly<LOGN, Q + 1, MIR>(t, b));
       static_for<R2>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
         // chunk c starts at r = c*R2/C, i.e. at index c*CS: the address is g + (r - c*R2/C)*(N/R2)
@@ -379,12 +411,12 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
   static_for<E>([&](auto ic) { v[decltype(ic)::value] = nv[decltype(ic)::value]; });
 }
 
-template <int LOGN, int Q, bool INV, int CH = kChunks[LOGN]>
+template <int LOGN, int Q, bool INV, int CH = kChunks[LOGN], bool MIR = false>
 __device__ __forceinline__ void stockham_from(float2* v, int t, float2* lds, const float2* __restrict__ tw) {
-  stockham_compute<LOGN, Q, INV>(v, t, tw);
+  stockham_compute<LOGN, Q, INV, MIR>(v, t, tw);
   if constexpr (Q + 1 < RowPlan<LOGN>::NP) {
-    stockham_exchange<LOGN, Q, CH>(v, t, lds);
-    stockham_from<LOGN, Q + 1, INV, CH>(v, t, lds, tw);
+    stockham_exchange<LOGN, Q, CH, MIR>(v, t, lds);
+    stockham_from<LOGN, Q + 1, INV, CH, MIR>(v, t, lds, tw);
   }
 }
 
@@ -418,9 +450,10 @@ __device__ __forceinline__ void load_forward(int t, const Src& src, typename Src
   }
 }
 
-template <int LOGN, bool DST_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN]>
+template <int LOGN, bool DST_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN], bool MIR = false>
 __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typename Src::raw_t* raw,
                                                    const Dst& dst, float2* lds, const float2* __restrict__ tw) {
+  static_assert(!MIR || (mirror_ok<LOGN>() && !DST_IN_LDS), "mirrored last pass: standalone rows only");
   using P = RowPlan<LOGN>;
   constexpr int N = P::N, E = P::E, TPR = P::TPR;
   if constexpr (LOGN == 0) {
@@ -432,12 +465,54 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
   } else {
     float2 v[E];
     static_for<E>([&](auto ic) { v[decltype(ic)::value] = Src::widen(raw[decltype(ic)::value]); });
-    stockham_from<LOGN, 0, false, CH>(v, t, lds, tw);
+    stockham_from<LOGN, 0, false, CH, MIR>(v, t, lds, tw);
 
     // Post-pass.  After the last pass thread t holds Z_m at m = g_b + r*(N/RL).
     constexpr int RL = radix(LOGN, P::NP - 1), BPL = E / RL, NsL = N / RL;
     constexpr int kPostOff = post_table_offset(LOGN);
     const float2* __restrict__ twp = tw + kPostOff;
+    if constexpr (MIR) {
+      // thread t holds butterfly g0 = t in v[0, RL) and g1 = N/RL - t in v[RL, 2 RL); thread
+      // 0 holds g0 = 0 and g1 = N/(2 RL), each of which pairs with itself
+      if (!active) return;
+      const bool z = t == 0;
+      const float2 tw0 = twp[t];  // -i W_n^t / 2
+      // thread 0's second butterfly: -i W_n^{NsL/2} / 2 times i (undoing the rotation by
+      // W_{2RL}^{RL/2} = -i that slot j >= RL/2 applies below) = W_{4RL} / 2
+      const float2 tw1 = z ? rot<4 * RL, 1, false>(make_float2(0.5f, 0.f)) : tw0;
+      static_for<RL>([&](auto jc) {
+        constexpr int j = decltype(jc)::value;
+        float2 a, pt, twj;
+        int k;
+        if constexpr (j < RL / 2) {
+          a = v[j];
+          pt = (j == 0 || !z) ? v[2 * RL - 1 - j] : v[RL - j];
+          k = t + j * NsL;
+          twj = tw0;
+        } else {
+          a = z ? v[RL + j - RL / 2] : v[j];
+          pt = z ? v[RL + 3 * RL / 2 - 1 - j] : v[2 * RL - 1 - j];
+          k = z ? NsL / 2 + (j - RL / 2) * NsL : t + j * NsL;
+          twj = tw1;
+        }
+        const float2 bc2 = c_conj(pt);
+        const float2 s = c_add(a, bc2), d = c_sub(a, bc2);
+        const float2 q = c_mul<false>(d, rot<2 * RL, j, false>(twj));
+        float2 lo = make_float2(fmaf(s.x, 0.5f, q.x), fmaf(s.y, 0.5f, q.y));
+        float2 hi = make_float2(fmaf(s.x, 0.5f, -q.x), -fmaf(s.y, 0.5f, -q.y));
+        int hi_idx = N - k;
+        if constexpr (j == 0) {
+          // thread 0: slot 0 = (Y_0, Y_{n/2}) and Y_{N/2} = conj(Z_{N/2}) (v[RL/2])
+          const float2 zh = c_conj(v[RL / 2]);
+          lo = z ? make_float2(a.x + a.y, a.x - a.y) : lo;
+          hi = z ? zh : hi;
+          hi_idx = z ? N / 2 : hi_idx;
+        }
+        dst.store(k, lo);
+        dst.store(hi_idx, hi);
+      });
+      return;
+    }
     float2 partner[E / 2];
     if constexpr (TPR == 1) {
       // the whole row is in this thread's registers: Z_{N-k} is v at N-k
@@ -521,12 +596,12 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
   }
 }
 
-template <int LOGN, bool DST_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN]>
+template <int LOGN, bool DST_IN_LDS, class Src, class Dst, int CH = kChunks[LOGN], bool MIR = false>
 __device__ __forceinline__ void row_forward(int t, bool active, const Src& src, const Dst& dst, float2* lds,
                                             const float2* __restrict__ tw) {
   typename Src::raw_t raw[RowPlan<LOGN>::E];
   load_forward<LOGN>(t, src, raw);
-  row_forward_loaded<LOGN, DST_IN_LDS, Src, Dst, CH>(t, active, raw, dst, lds, tw);
+  row_forward_loaded<LOGN, DST_IN_LDS, Src, Dst, CH, MIR>(t, active, raw, dst, lds, tw);
 }
 
 // ----------------------------------------------------------------------------------

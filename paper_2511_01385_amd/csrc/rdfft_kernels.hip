@@ -33,7 +33,7 @@ __global__ void __launch_bounds__(RowPlan<LOGN>::WG) rdfft_rows_kernel(Elem* buf
   const bool active = row < rows;
   const Acc acc{buf + (active ? row : 0) * (int64_t)P::N};
   float2* my = lds + rho * LDS_ROW;
-  if constexpr (!INV) row_forward<LOGN, false, Acc, Acc, CH>(t, active, acc, acc, my, tw);
+  if constexpr (!INV) row_forward<LOGN, false, Acc, Acc, CH, mirror_ok<LOGN>()>(t, active, acc, acc, my, tw);
   else row_inverse<LOGN, false, Acc, Acc, CH>(t, active, acc, acc, my, tw);
 }
 
