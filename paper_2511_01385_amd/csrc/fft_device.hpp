@@ -301,10 +301,9 @@ struct RowPlan {
 // can take butterflies t and N/RL - t (thread 0: 0 and N/(2 RL)).  Bin k = g + r N/RL of
 // butterfly g and its post-pass partner N - k then sit in the same thread, and the forward
 // post-pass needs no LDS exchange.  Only the standalone row kernels use it: the layer
-// kernels read the spectrum in the plain order.  It costs ~5% more VALU instructions (the
+// kernels read the spectrum in the plain order.  It costs ~2% more VALU instructions (the
 // selects for thread 0) for one LDS round trip and one barrier fewer: timed, that pays for
-// n >= 2048 (1-2%) and not for n = 64 or 256 (8-12% slower), so shorter rows keep the
-// exchange.
+// n >= 2048 and not for n = 64 or 256, so shorter rows keep the exchange.
 template <int LOGN>
 constexpr bool mirror_ok() {
   using P = RowPlan<LOGN>;
@@ -477,9 +476,12 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
       if (!active) return;
       const bool z = t == 0;
       const float2 tw0 = twp[t];  // -i W_n^t / 2
-      // thread 0's second butterfly: -i W_n^{NsL/2} / 2 times i (undoing the rotation by
-      // W_{2RL}^{RL/2} = -i that slot j >= RL/2 applies below) = W_{4RL} / 2
-      const float2 tw1 = z ? rot<4 * RL, 1, false>(make_float2(0.5f, 0.f)) : tw0;
+      // slots j >= RL/2: other threads pair v[j] (bin t + j N/RL) with v[2RL-1-j]; thread 0
+      // pairs v[RL + j] (bin N/(2RL) + j N/RL of its second butterfly) with the same v[2RL-1-j],
+      // so only the first operand, the twiddle (-i W_n^{N/(2RL)} / 2 = -i W_{4RL} / 2) and
+      // the bins' base differ
+      const float2 tw1 = z ? rot<4 * RL, 1, false>(make_float2(0.f, -0.5f)) : tw0;
+      const int kb1 = z ? NsL / 2 : t;
       static_for<RL>([&](auto jc) {
         constexpr int j = decltype(jc)::value;
         float2 a, pt, twj;
@@ -490,9 +492,9 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
           k = t + j * NsL;
           twj = tw0;
         } else {
-          a = z ? v[RL + j - RL / 2] : v[j];
-          pt = z ? v[RL + 3 * RL / 2 - 1 - j] : v[2 * RL - 1 - j];
-          k = z ? NsL / 2 + (j - RL / 2) * NsL : t + j * NsL;
+          a = z ? v[RL + j] : v[j];
+          pt = v[2 * RL - 1 - j];
+          k = kb1 + j * NsL;
           twj = tw1;
         }
         const float2 bc2 = c_conj(pt);
