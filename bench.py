@@ -234,6 +234,24 @@ def copy_rate(dev, stream, reps: int = 5):
     return round(2 * POOL_BYTES / us / 1e3, 1)
 
 
+def inplace_rate(dev, stream, reps: int = 5):
+    """Read+write GB/s of an in-place elementwise pass (negation) over 1 GiB of bf16 on this GPU:
+    the same access pattern as an in-place row transform, without its arithmetic."""
+    import torch
+
+    a = torch.ones(POOL_BYTES // 2, dtype=torch.bfloat16, device=dev)
+    a.mul_(-1.0)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        a.mul_(-1.0)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    del a
+    return round(2 * POOL_BYTES / us / 1e3, 1)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -401,6 +419,9 @@ def main():
     copy_gbs = copy_rate(dev, stream)
     out["hbm_copy"] = {"GB_s": copy_gbs, "frac_of_copy": round(value / copy_gbs, 4),
                        "roofline_frac_of_copy": round(dom["GB_s"] / copy_gbs, 4)}
+    inplace_gbs = inplace_rate(dev, stream)
+    out["hbm_inplace"] = {"GB_s": inplace_gbs, "frac_of_inplace": round(value / inplace_gbs, 4),
+                          "roofline_frac_of_inplace": round(dom["GB_s"] / inplace_gbs, 4)}
     if not args.no_configs:
         del pools, sets
         torch.cuda.empty_cache()
