@@ -279,6 +279,39 @@ def test_special_inputs_closed_forms():
     np.testing.assert_allclose(got, want, atol=2e-3)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n", [2048, 4096])
+def test_single_bin_closed_forms_long_rows(n, dtype):
+    """cos and sin rows with one frequency k0 give Y_k0 = n/2 and -i n/2 (and zero elsewhere) for
+    0 < k0 < n/2.  The frequencies cover the first and last bins of every group of N/8 pair slots
+    (N = n/2), the quarter and half points, and bins next to them, so each bin position of the
+    transform's last radix-8 pass and of its partner N - k is checked against the definition."""
+    N = n // 2
+    s = N // 8
+    ks = sorted({k for j in range(8) for k in (j * s, j * s + s // 2, j * s + s // 2 + 1, j * s - 1) if 0 < k < N}
+                | {N // 2, N // 2 - 1, 1, N - 1})
+    m = np.arange(n)
+    rows = []
+    want = []
+    for k0 in ks:
+        for kind in ("cos", "sin"):
+            rows.append(np.cos(2 * np.pi * k0 * m / n) if kind == "cos" else np.sin(2 * np.pi * k0 * m / n))
+            w = np.zeros(n)
+            if kind == "cos":
+                w[2 * k0] = n / 2
+            else:
+                w[2 * k0 + 1] = -n / 2
+            want.append(w)
+    t = to_device(inputs.round_to(np.array(rows), dtype), dtype)
+    api.rdfft_forward(t)
+    torch.cuda.synchronize()
+    got = to_host_f64(t)
+    # f32 rows: the DFT of the rounded inputs is the closed form to ~1e-6 n; bf16 rows carry
+    # input rounding (relative 2^-9 per sample) and a bf16 store of the output (n/2 lands within n/512)
+    atol = 2e-5 * n if dtype == "f32" else 0.004 * n  # bf16: half an ulp of n/2 is n/512
+    np.testing.assert_allclose(got, np.array(want), atol=atol)
+
+
 @pytest.mark.parametrize("n", [1024, 3000])
 def test_no_device_allocation(n):
     x = to_device(inputs.normal_rows(9, 4096, n, "bf16"), "bf16")
