@@ -280,15 +280,17 @@ def test_special_inputs_closed_forms():
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("n", [2048, 4096])
-def test_single_bin_closed_forms_long_rows(n, dtype):
+@pytest.mark.parametrize("n,last_radix", [(2048, 8), (4096, 8), (65536, 32)])
+def test_single_bin_closed_forms_long_rows(n, last_radix, dtype):
     """cos and sin rows with one frequency k0 give Y_k0 = n/2 and -i n/2 (and zero elsewhere) for
-    0 < k0 < n/2.  The frequencies cover the first and last bins of every group of N/8 pair slots
-    (N = n/2), the quarter and half points, and bins next to them, so each bin position of the
-    transform's last radix-8 pass and of its partner N - k is checked against the definition."""
+    0 < k0 < n/2.  The frequencies cover the first and last bins of every group of N/R pair slots
+    (N = n/2, R the radix of the transform's last pass), the middle of each group, the quarter
+    and half points, and bins next to them, so each bin position of the last pass and of its
+    partner N - k is checked against the definition."""
     N = n // 2
-    s = N // 8
-    ks = sorted({k for j in range(8) for k in (j * s, j * s + s // 2, j * s + s // 2 + 1, j * s - 1) if 0 < k < N}
+    s = N // last_radix
+    ks = sorted({k for j in range(last_radix) for k in (j * s, j * s + s // 2, j * s + s // 2 + 1, j * s - 1)
+                 if 0 < k < N}
                 | {N // 2, N // 2 - 1, 1, N - 1})
     m = np.arange(n)
     rows = []
