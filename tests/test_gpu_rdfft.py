@@ -279,22 +279,18 @@ def test_special_inputs_closed_forms():
     np.testing.assert_allclose(got, want, atol=2e-3)
 
 
-@pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("n,last_radix", [(2048, 8), (4096, 8), (65536, 32)])
-def test_single_bin_closed_forms_long_rows(n, last_radix, dtype):
-    """cos and sin rows with one frequency k0 give Y_k0 = n/2 and -i n/2 (and zero elsewhere) for
-    0 < k0 < n/2.  The frequencies cover the first and last bins of every group of N/R pair slots
-    (N = n/2, R the radix of the transform's last pass), the middle of each group, the quarter
-    and half points, and bins next to them, so each bin position of the last pass and of its
-    partner N - k is checked against the definition."""
+def _single_bin_rows(n, last_radix):
+    """cos and sin rows of one frequency k0 each, and their packed spectra: Y_k0 = n/2 (cos) or
+    -i n/2 (sin), zero elsewhere, for 0 < k0 < n/2.  The frequencies cover the first and last
+    bins of every group of N/R pair slots (N = n/2, R the radix of the transform's last pass),
+    the middle of each group, the quarter and half points, and bins next to them, so every bin
+    position of the last pass, and of its partner N - k, is met."""
     N = n // 2
     s = N // last_radix
     ks = sorted({k for j in range(last_radix) for k in (j * s, j * s + s // 2, j * s + s // 2 + 1, j * s - 1)
-                 if 0 < k < N}
-                | {N // 2, N // 2 - 1, 1, N - 1})
+                 if 0 < k < N} | {N // 2, N // 2 - 1, 1, N - 1})
     m = np.arange(n)
-    rows = []
-    want = []
+    rows, spectra = [], []
     for k0 in ks:
         for kind in ("cos", "sin"):
             rows.append(np.cos(2 * np.pi * k0 * m / n) if kind == "cos" else np.sin(2 * np.pi * k0 * m / n))
@@ -303,15 +299,38 @@ def test_single_bin_closed_forms_long_rows(n, last_radix, dtype):
                 w[2 * k0] = n / 2
             else:
                 w[2 * k0 + 1] = -n / 2
-            want.append(w)
-    t = to_device(inputs.round_to(np.array(rows), dtype), dtype)
+            spectra.append(w)
+    return np.array(rows), np.array(spectra)
+
+
+LONG_ROW_LAST_RADIX = [(2048, 8), (4096, 8), (65536, 32)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,last_radix", LONG_ROW_LAST_RADIX)
+def test_single_bin_closed_forms_long_rows(n, last_radix, dtype):
+    """The forward of single-frequency rows is the closed-form spectrum."""
+    rows, spectra = _single_bin_rows(n, last_radix)
+    t = to_device(inputs.round_to(rows, dtype), dtype)
     api.rdfft_forward(t)
     torch.cuda.synchronize()
-    got = to_host_f64(t)
     # f32 rows: the DFT of the rounded inputs is the closed form to ~1e-6 n; bf16 rows carry
     # input rounding (relative 2^-9 per sample) and a bf16 store of the output (n/2 lands within n/512)
-    atol = 2e-5 * n if dtype == "f32" else 0.004 * n  # bf16: half an ulp of n/2 is n/512
-    np.testing.assert_allclose(got, np.array(want), atol=atol)
+    atol = 2e-5 * n if dtype == "f32" else 0.004 * n
+    np.testing.assert_allclose(to_host_f64(t), spectra, atol=atol)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,last_radix", LONG_ROW_LAST_RADIX)
+def test_single_bin_inverse_closed_forms_long_rows(n, last_radix, dtype):
+    """The inverse of a single-bin spectrum (exact in either storage type) is the cos or sin row."""
+    rows, spectra = _single_bin_rows(n, last_radix)
+    t = to_device(inputs.round_to(spectra, dtype), dtype)
+    api.rdfft_inverse(t)
+    torch.cuda.synchronize()
+    # unit-amplitude outputs: f32 arithmetic error ~1e-6; bf16 adds one rounding (2^-9 relative)
+    atol = 1e-5 if dtype == "f32" else 4e-3
+    np.testing.assert_allclose(to_host_f64(t), rows, atol=atol)
 
 
 @pytest.mark.parametrize("n", [1024, 3000])
