@@ -244,3 +244,61 @@ def test_no_device_allocation(tokens, d, p):
     torch.cuda.synchronize()
     assert torch.cuda.memory_allocated() == alloc0
     assert torch.cuda.mem_get_info()[0] == free0
+
+
+def _impulse_spectra(shifts, p):
+    """Packed spectra of impulse circulants c_ij = e_{s_ij} (s < 0: a zero block), from the closed
+    form Y_k = exp(-2 pi i k s / p): slot 0 holds (1, (-1)^s), slot k (cos, -sin)(2 pi k s / p)."""
+    q, kb = shifts.shape
+    out = np.zeros((q, kb, p))
+    k = np.arange(1, p // 2)
+    for i in range(q):
+        for j in range(kb):
+            s = shifts[i, j]
+            if s < 0:
+                continue
+            out[i, j, 0] = 1.0
+            out[i, j, 1] = (-1.0) ** s
+            out[i, j, 2::2] = np.cos(2 * np.pi * k * s / p)
+            out[i, j, 3::2] = -np.sin(2 * np.pi * k * s / p)
+    return out
+
+
+@pytest.mark.parametrize("tokens,d,p,dtype", [(37, 256, 64, "f32"), (64, 768, 256, "bf16"), (96, 4096, 1024, "bf16"),
+                                              (48, 8192, 8192, "bf16"), (8, 65536, 65536, "f32")],
+                         ids=["p64_f32", "p256_bf16", "p1024_bf16", "p8192_bf16", "p65536_f32"])
+def test_impulse_circulants_shift(tokens, d, p, dtype):
+    """With c_ij an impulse at s_ij the layer is a sum of circular shifts, by the definition of a
+    circulant (first column c): y_i = sum_j roll(x_j, s_ij) and dx_j = sum_i roll(g_i, -s_ij).
+    The spectra are the impulses' closed-form transforms (no oracle, no library transform)."""
+    q = d // p
+    rng = np.random.default_rng(2511 + p)
+    shifts = rng.integers(0, p, size=(q, q))
+    shifts[rng.random((q, q)) < 0.3] = -1  # some zero blocks
+    spectra = _impulse_spectra(shifts, p)
+    x = rng.standard_normal((tokens, d))
+    g = rng.standard_normal((tokens, d))
+    xs, gs, cs = (inputs.round_to(a, dtype) for a in (x, g, spectra))
+    xt, gt, ct = to_device(xs, dtype), to_device(gs, dtype), to_device(cs, dtype)
+    yt = torch.empty((tokens, d), dtype=TORCH_DTYPE[dtype], device="cuda")
+    dxt = torch.empty_like(yt)
+    dct = torch.empty((q, q, p), dtype=torch.float32, device="cuda")
+    api.bca_forward(xt, ct, yt)
+    api.bca_backward(xt, ct, gt, dxt, dct)
+    torch.cuda.synchronize()
+    x64, g64 = inputs.to_f64(xs, dtype).reshape(tokens, q, p), inputs.to_f64(gs, dtype).reshape(tokens, q, p)
+    y_ref = np.zeros((tokens, q, p))
+    dx_ref = np.zeros((tokens, q, p))
+    for i in range(q):
+        for j in range(q):
+            s = shifts[i, j]
+            if s >= 0:
+                y_ref[:, i] += np.roll(x64[:, j], s, axis=1)
+                dx_ref[:, j] += np.roll(g64[:, i], -s, axis=1)
+    # the stored spectra are the impulses' transforms rounded to the storage type, so the effective
+    # circulants are impulses up to that rounding: the storage type's relative bar applies
+    bar = 1e-5 if dtype == "f32" else 2e-2
+    for name, got, ref in (("y", yt, y_ref), ("dx", dxt, dx_ref)):
+        got = to_host_f64(got).reshape(ref.shape)
+        err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+        assert err <= bar, f"{name}: rel-L2 {err:.3e} > {bar}"
