@@ -270,7 +270,8 @@ def _impulse_spectra(shifts, p):
 def test_impulse_circulants_shift(tokens, d, p, dtype):
     """With c_ij an impulse at s_ij the layer is a sum of circular shifts, by the definition of a
     circulant (first column c): y_i = sum_j roll(x_j, s_ij) and dx_j = sum_i roll(g_i, -s_ij).
-    The spectra are the impulses' closed-form transforms (no oracle, no library transform)."""
+    The spectra are the impulses' closed-form transforms (no oracle, no library transform), and
+    dc is checked against the cross-correlation theorem with NumPy's float64 FFT."""
     q = d // p
     rng = np.random.default_rng(2511 + p)
     shifts = rng.integers(0, p, size=(q, q))
@@ -302,3 +303,12 @@ def test_impulse_circulants_shift(tokens, d, p, dtype):
         got = to_host_f64(got).reshape(ref.shape)
         err = np.linalg.norm(got - ref) / np.linalg.norm(ref)
         assert err <= bar, f"{name}: rel-L2 {err:.3e} > {bar}"
+    # dc does not depend on c: dc_ij[r] = sum_t sum_m g_i[m] x_j[m - r], a circular
+    # cross-correlation, i.e. sum_t IDFT(DFT(g_i) conj(DFT(x_j))); float32 arithmetic on exactly
+    # widened inputs, except that blocks beyond 8192 store their spectra in the storage type
+    G, X = np.fft.rfft(g64, axis=2), np.fft.rfft(x64, axis=2)
+    dc_ref = np.fft.irfft(np.einsum("tik,tjk->ijk", G, np.conj(X)), n=p, axis=2)
+    dc_bar = 2e-2 if (dtype == "bf16" and p > 8192) else 1e-5
+    got = dct.cpu().numpy().astype(np.float64)
+    err = np.linalg.norm(got - dc_ref) / np.linalg.norm(dc_ref)
+    assert err <= dc_bar, f"dc: rel-L2 {err:.3e} > {dc_bar}"
