@@ -48,3 +48,6 @@ def test_short_run_prints_one_complete_json_line():
     # value is the whole step's bytes over its time
     assert abs(d["value"] - d["config"]["bytes_per_step"] / (d["ms_per_step"] * 1e6)) / d["value"] < 0.01
     assert d["aux_bytes"] == 0
+    # the reference rates beside the roofline: a device copy and an in-place pass over 1 GiB
+    for ref in ("hbm_copy", "hbm_inplace"):
+        assert d[ref]["GB_s"] > 0, ref
