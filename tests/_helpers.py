@@ -81,3 +81,21 @@ def sample_rows(rows: int, count: int, seed: int) -> np.ndarray:
     rng = np.random.default_rng(seed)
     pick = rng.choice(rows, size=min(count, rows), replace=False)
     return np.unique(np.concatenate([pick, [0, rows - 1]]))
+
+
+def impulse_spectra(shifts, p):
+    """Packed spectra of impulse circulants c_ij = e_{s_ij} (s < 0: a zero block), from the closed
+    form Y_k = exp(-2 pi i k s / p): slot 0 holds (1, (-1)^s), slot k (cos, -sin)(2 pi k s / p)."""
+    q, kb = shifts.shape
+    out = np.zeros((q, kb, p))
+    k = np.arange(1, p // 2)
+    for i in range(q):
+        for j in range(kb):
+            s = shifts[i, j]
+            if s < 0:
+                continue
+            out[i, j, 0] = 1.0
+            out[i, j, 1] = (-1.0) ** s
+            out[i, j, 2::2] = np.cos(2 * np.pi * k * s / p)
+            out[i, j, 3::2] = -np.sin(2 * np.pi * k * s / p)
+    return out

@@ -12,7 +12,7 @@ import torch
 
 from oracle import bca as obca
 from paper_2511_01385_amd import api, inputs
-from tests._helpers import ELEMENT_REL, TORCH_DTYPE, assert_close, to_device, to_host_f64
+from tests._helpers import ELEMENT_REL, TORCH_DTYPE, assert_close, impulse_spectra, to_device, to_host_f64
 
 pytestmark = pytest.mark.gpu
 
@@ -246,24 +246,6 @@ def test_no_device_allocation(tokens, d, p):
     assert torch.cuda.mem_get_info()[0] == free0
 
 
-def _impulse_spectra(shifts, p):
-    """Packed spectra of impulse circulants c_ij = e_{s_ij} (s < 0: a zero block), from the closed
-    form Y_k = exp(-2 pi i k s / p): slot 0 holds (1, (-1)^s), slot k (cos, -sin)(2 pi k s / p)."""
-    q, kb = shifts.shape
-    out = np.zeros((q, kb, p))
-    k = np.arange(1, p // 2)
-    for i in range(q):
-        for j in range(kb):
-            s = shifts[i, j]
-            if s < 0:
-                continue
-            out[i, j, 0] = 1.0
-            out[i, j, 1] = (-1.0) ** s
-            out[i, j, 2::2] = np.cos(2 * np.pi * k * s / p)
-            out[i, j, 3::2] = -np.sin(2 * np.pi * k * s / p)
-    return out
-
-
 @pytest.mark.parametrize("tokens,d,p,dtype", [(37, 256, 64, "f32"), (64, 768, 256, "bf16"), (96, 4096, 1024, "bf16"),
                                               (48, 8192, 8192, "bf16"), (8, 65536, 65536, "f32")],
                          ids=["p64_f32", "p256_bf16", "p1024_bf16", "p8192_bf16", "p65536_f32"])
@@ -276,7 +258,7 @@ def test_impulse_circulants_shift(tokens, d, p, dtype):
     rng = np.random.default_rng(2511 + p)
     shifts = rng.integers(0, p, size=(q, q))
     shifts[rng.random((q, q)) < 0.3] = -1  # some zero blocks
-    spectra = _impulse_spectra(shifts, p)
+    spectra = impulse_spectra(shifts, p)
     x = rng.standard_normal((tokens, d))
     g = rng.standard_normal((tokens, d))
     xs, gs, cs = (inputs.round_to(a, dtype) for a in (x, g, spectra))

@@ -164,3 +164,19 @@ def test_block_size_must_divide():
     x = np.zeros((2, 12))
     with pytest.raises(ValueError):
         bca.forward_spectral(x, np.zeros((1, 1, 8)), 8, 8)
+
+
+def test_impulse_spectra_helper_matches_oracle():
+    """The closed-form impulse spectra that the GPU layer tests feed the library equal the oracle's
+    packed transform of the impulse columns (zero blocks stay zero)."""
+    from tests._helpers import impulse_spectra
+
+    for p in (2, 4, 64, 256):
+        shifts = np.array([[0, 1, -1], [p - 1, p // 2, 3 % p]])
+        got = impulse_spectra(shifts, p)
+        for i in range(shifts.shape[0]):
+            for j in range(shifts.shape[1]):
+                col = np.zeros(p)
+                if shifts[i, j] >= 0:
+                    col[shifts[i, j]] = 1.0
+                np.testing.assert_allclose(got[i, j], rd.rdfft_forward(col[None])[0], atol=1e-12)
