@@ -54,7 +54,7 @@ typedef struct ihipStream_t *rdfft_stream_t;
 typedef enum {
   RDFFT_F32 = 0,  /* IEEE float32 storage */
   RDFFT_BF16 = 1, /* bfloat16 storage */
-  RDFFT_F16 = 2   /* IEEE float16 storage: transforms and layout converters only */
+  RDFFT_F16 = 2   /* IEEE float16 storage */
 } rdfft_dtype_t;
 
 typedef enum {
@@ -126,13 +126,14 @@ typedef struct {
  *              d_in == d_out (a truly in-place layer, Sec. 5.1.1); any other
  *              overlap with x or c_spectra -> RDFFT_EINVAL.
  *   grads      reserved, must be NULL.
- *   dtype      RDFFT_F32 or RDFFT_BF16 (RDFFT_F16 -> RDFFT_EUNSUPPORTED).
+ *   dtype      RDFFT_F32, RDFFT_BF16 or RDFFT_F16: the storage of x, c_spectra and y
+ *              (float32 arithmetic; 16-bit stores round to nearest even).
  *   p          power of two, 2 <= p <= 65536 (larger -> RDFFT_EUNSUPPORTED);
  *              must divide d_in and d_out (Table 1 marks such shapes N/A) -> else RDFFT_EINVAL.
  *   tokens     >= 0; 0 is a no-op (x and y may then be NULL).
  * Blocks beyond 8192 (p = 16384, 32768, 65536) run as passes over HBM that stage the
  * input spectra in y: they need kb <= q and kb <= 8 (else RDFFT_EUNSUPPORTED), and the
- * staged spectra are stored in dtype (for bf16 one more rounding of each spectrum).
+ * staged spectra are stored in dtype (for 16-bit storage one more rounding of each spectrum).
  */
 RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_grads_t *grads, int64_t d_in,
                 int64_t d_out, int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream);

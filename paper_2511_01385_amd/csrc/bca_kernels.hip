@@ -1,553 +1,18 @@
-// bca_kernels.hip -- fused block-circulant layer kernels (Sec. 3.3, Eqs. (4)-(5)).
-//
-// A workgroup takes a tile of TT tokens at a time and keeps every spectrum of the
-// tile in LDS, in the packed pair layout of the row transforms:
-//   forward : X_j = rdFFT(x_j)  ->  Y_i = sum_j C_ij . X_j  ->  y_i = irdFFT(Y_i)
-//   backward: X_j = rdFFT(x_j), G_i = rdFFT(g_i)
-//             dC_ij += conj(X_j) . G_i          (float32 partial sums in LDS)
-//             dX_j   = sum_i conj(C_ij) . G_i  ->  dx_j = irdFFT(dX_j)
-// so no intermediate tensor ever reaches HBM.  Slot 0 of a packed spectrum holds
-// the two real bins Y_0 and Y_{p/2}; every product acts on them as two real
-// products (conjugation is the identity there).  The backward runs one wide persistent
-// workgroup per CU; its dC partial sums stay in LDS (or registers) for all of its tiles
-// and are then added into the caller's dc buffer with float32 atomics (each workgroup
-// starting at a different offset), or, for the square-layer kernel when dx is not gy,
-// staged in the gy rows the workgroup has consumed and summed by a second kernel; a final
-// in-place irdFFT of dc (stream-ordered after the kernels) yields the time-domain
-// gradient.  A single circulant of p = 8192 and blocks beyond 8192 are routed to the row
-// kernels of bca_multipass.hip.
+// bca_kernels.hip -- dispatch of the fused block-circulant layer (Sec. 3.3, Eqs. (4)-(5))
+// to the kernels of bca_kernels.hpp (instantiated per storage type in
+// bca_store_{f32,bf16,f16}.hip) and the multi-pass layer of bca_multipass.hip, plus the
+// two small kernels every storage type shares: the fill of dc and the second stage of
+// the two-stage dC sum.
 #include <hip/hip_runtime.h>
 
-#include "fft_device.hpp"
-#include "launch.hpp"
+#include "bca_kernels.hpp"
 
 namespace rdfft {
-
-template <int LOGN>
-struct BcaPlan {
-  using P = RowPlan<LOGN>;
-  static constexpr int N = P::N;
-  static constexpr int TPR = P::TPR;
-  static_assert(TPR <= 256, "row too long for the fused layer kernels");
-  // forward: 256 threads, or two row groups for the longest rows
-  static constexpr int FWD_WG = 2 * TPR > 256 ? 2 * TPR : 256;
-  // backward: one wide workgroup per CU keeps the number of dC partial sums (and so
-  // of atomics) small; 1024 threads when the plan is light on registers
-  static constexpr int BWD_WG = (P::E <= 8 && TPR <= 128) ? 1024 : 512;
-  static constexpr int REGION = P::LDS_F2 > lds_padded_size(N) ? P::LDS_F2 : lds_padded_size(N);
-};
-
-// acc + a.b (or acc + conj(a).b) on packed pair slots.  Slot 0 (S0) holds the two real
-// bins Y_0 and Y_{p/2}: there the product is two real products and conj is the identity.
-template <bool S0, bool CONJ>
-__device__ __forceinline__ float2 slot_mac(float2 acc, float2 a, float2 b) {
-  if constexpr (S0) return make_float2(fmaf(a.x, b.x, acc.x), fmaf(a.y, b.y, acc.y));
-  if constexpr (!CONJ) return make_float2(fmaf(a.x, b.x, fmaf(-a.y, b.y, acc.x)), fmaf(a.x, b.y, fmaf(a.y, b.x, acc.y)));
-  return make_float2(fmaf(a.x, b.x, fmaf(a.y, b.y, acc.x)), fmaf(a.x, b.y, fmaf(-a.y, b.x, acc.y)));
-}
-
-template <class Elem>
-struct Acc;
-template <>
-struct Acc<float2> {
-  using In = ConstF32;
-  using Out = GlobalF32;
-};
-template <>
-struct Acc<uint32_t> {
-  using In = ConstBF16;
-  using Out = GlobalBF16;
-};
-
-extern __shared__ float2 bca_lds[];
-
-// x: [T][kb*N] pairs, c: [q][kb][N] pairs, y: [T][q*N] pairs (all in storage type Elem)
-template <int LOGN, class Elem, int WG = BcaPlan<LOGN>::FWD_WG>
-__global__ void __launch_bounds__(WG) bca_forward_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
-                                                                  Elem* y, int64_t tokens, int q, int kb, int tt_per_tile,
-                                                                  const float2* __restrict__ tw) {
-  using B = BcaPlan<LOGN>;
-  using In = typename Acc<Elem>::In;
-  using Out = typename Acc<Elem>::Out;
-  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
-  const int tid = threadIdx.x;
-  const int grp = tid / TPR, t = tid - grp * TPR;
-  const int TT = tt_per_tile;
-  float2* const xs = bca_lds;                        // TT*kb regions
-  float2* const ys = bca_lds + (size_t)TT * kb * REG;  // TT*q regions
-  float2* const dummy = bca_lds + (size_t)TT * (kb + q) * REG;
-  const int64_t tok0 = (int64_t)blockIdx.x * TT;
-
-  // Phase A: X_j = rdFFT(x_j) for every (token, j) of the tile, into LDS
-  const int nx = TT * kb;
-  for (int s0 = 0; s0 < nx; s0 += NG) {
-    const int s = s0 + grp;
-    const bool valid = s < nx;
-    const int tt = valid ? s / kb : 0, j = valid ? s - tt * kb : 0;
-    const bool act = valid && tok0 + tt < tokens;
-    float2* reg = valid ? xs + (size_t)s * REG : dummy;
-    const In src{x + ((act ? tok0 + tt : 0) * kb + j) * (int64_t)N};
-    row_forward<LOGN, true>(t, act, src, LdsSpectrum{reg}, reg, tw);
-  }
-  __syncthreads();
-
-  // Phase B: Y_i[k] = sum_j C_ij[k] . X_j[k]; a thread takes one (token, bin) and all i, j.
-  // Bin 0 is slot 0 and takes the branch with real products (one lane of one wave).
-  const In cin{c};
-  for (int it = tid; it < TT * N; it += WG) {
-    const int tt = it / N, k = it - tt * N;
-    const float2* xk = xs + (size_t)tt * kb * REG + lds_pad(k);
-    float2* yk = ys + (size_t)tt * q * REG + lds_pad(k);
-    auto block_sum = [&](auto s0c) {
-      constexpr bool S0 = decltype(s0c)::value;
-      int ci = k;  // pair index of C_ij[k] = (i*kb + j)*N + k
-      for (int i = 0; i < q; ++i) {
-        float2 a = make_float2(0.f, 0.f);
-        // unrolled so that several L2 loads of C are in flight at once
-#pragma unroll 4
-        for (int j = 0; j < kb; ++j) a = slot_mac<S0, false>(a, cin.load(ci + j * N), xk[j * REG]);
-        ci += kb * N;
-        yk[i * REG] = a;
-      }
-    };
-    if (k == 0) block_sum(std::true_type{});
-    else block_sum(std::false_type{});
-  }
-  __syncthreads();
-
-  // Phase C: y_i = irdFFT(Y_i)
-  const int ny = TT * q;
-  for (int s0 = 0; s0 < ny; s0 += NG) {
-    const int s = s0 + grp;
-    const bool valid = s < ny;
-    const int tt = valid ? s / q : 0, i = valid ? s - tt * q : 0;
-    const bool act = valid && tok0 + tt < tokens;
-    float2* reg = valid ? ys + (size_t)s * REG : dummy;
-    const Out dst{y + ((act ? tok0 + tt : 0) * q + i) * (int64_t)N};
-    row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, tw);
-  }
-}
-
-// General backward.  gy: [T][q*N] pairs (read), dx: [T][kb*N] pairs (written; may alias
-// gy when kb == q), dc: [q][kb][N] float2 slots, receives spectral partial sums (atomically).
-// A launch covers the output blocks i0 <= i < i0+ia and input blocks j0 <= j < j0+jb and
-// does the dx path (mode & kBwdDx; needs every block: i0 = j0 = 0, ia = q, jb = kb), the dC
-// accumulation (mode & kBwdDc), or both.  Layers whose q*kb*(p/2) dC slots do not fit
-// in LDS run one dx launch and then dC launches over block ranges that do.
-constexpr int kBwdDx = 1, kBwdDc = 2;
-
-template <int LOGN, class Elem, int WG = BcaPlan<LOGN>::BWD_WG>
-__global__ void __launch_bounds__(WG) bca_backward_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
-                                                                   const Elem* gy, Elem* dx, float* __restrict__ dc,
-                                                                   int64_t tokens, int q, int kb, int i0, int ia,
-                                                                   int j0, int jb, int mode, int tt_per_tile,
-                                                                   int64_t ntiles, const float2* __restrict__ tw) {
-  using B = BcaPlan<LOGN>;
-  using In = typename Acc<Elem>::In;
-  using Out = typename Acc<Elem>::Out;
-  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
-  const int tid = threadIdx.x;
-  const int grp = tid / TPR, t = tid - grp * TPR;
-  const int TT = tt_per_tile;
-  const bool do_dx = (mode & kBwdDx) != 0, do_dc = (mode & kBwdDc) != 0;
-  float2* const xs = bca_lds;                        // TT*jb regions: X, then dX
-  float2* const gs = bca_lds + (size_t)TT * jb * REG;  // TT*ia regions: G
-  float2* const dummy = bca_lds + (size_t)TT * (jb + ia) * REG;
-  float2* const acc = dummy + REG;                   // ia*jb*N dC partial sums (pair slots)
-  const int qkn = do_dc ? ia * jb * N : 0;
-  const In cin{c};
-
-  for (int e = tid; e < qkn; e += WG) acc[e] = make_float2(0.f, 0.f);
-
-  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    const int64_t tok0 = tile * TT;
-    const int nvalid = (int)(tokens - tok0 < TT ? tokens - tok0 : TT);
-
-    // Phase A: X_j = rdFFT(x_j), G_i = rdFFT(g_i) for the launch's blocks
-    const int nx = TT * jb, ns = TT * (jb + ia);
-    for (int s0 = 0; s0 < ns; s0 += NG) {
-      const int s = s0 + grp;
-      const bool valid = s < ns;
-      float2* reg = valid ? bca_lds + (size_t)s * REG : dummy;
-      // choose the source without branching around the transform: its barriers
-      // must be reached by every lane of every wave
-      const Elem* srcp = x;
-      bool act = false;
-      if (valid && s < nx) {
-        const int tt = s / jb, j = j0 + s - tt * jb;
-        act = tt < nvalid;
-        srcp = x + ((act ? tok0 + tt : 0) * kb + j) * (int64_t)N;
-      } else if (valid) {
-        const int sg = s - nx;
-        const int tt = sg / ia, i = i0 + sg - tt * ia;
-        act = tt < nvalid;
-        srcp = gy + ((act ? tok0 + tt : 0) * q + i) * (int64_t)N;
-      }
-      row_forward<LOGN, true>(t, act, In{srcp}, LdsSpectrum{reg}, reg, tw);
-    }
-    __syncthreads();
-
-    // Phase B1: dC_ij[k] += sum_t conj(X_tj[k]) . G_ti[k]; each slot has one owner thread
-    for (int e = tid; e < qkn; e += WG) {
-      const int k = e & (N - 1);
-      const int ij = e / N;
-      const int ii = ij / jb, jj = ij - ii * jb;
-      const float2* xp = xs + (size_t)jj * REG + lds_pad(k);
-      const float2* gp = gs + (size_t)ii * REG + lds_pad(k);
-      auto contract = [&](auto s0c) {
-        constexpr bool S0 = decltype(s0c)::value;
-        float2 sum = acc[e];
-#pragma unroll 4
-        for (int tt = 0; tt < nvalid; ++tt) sum = slot_mac<S0, true>(sum, xp[(size_t)tt * jb * REG], gp[(size_t)tt * ia * REG]);
-        acc[e] = sum;
-      };
-      if (k == 0) contract(std::true_type{});
-      else contract(std::false_type{});
-    }
-    if (!do_dx) {
-      __syncthreads();
-      continue;
-    }
-    __syncthreads();
-
-    // Phase B2: dX_j[k] = sum_i conj(C_ij[k]) . G_i[k], written over X_j
-    for (int it = tid; it < TT * N; it += WG) {
-      const int tt = it / N, k = it - tt * N;
-      const float2* gk = gs + (size_t)tt * q * REG + lds_pad(k);
-      float2* xk = xs + (size_t)tt * kb * REG + lds_pad(k);
-      auto grad_x = [&](auto s0c) {
-        constexpr bool S0 = decltype(s0c)::value;
-        for (int j = 0; j < kb; ++j) {
-          float2 a = make_float2(0.f, 0.f);
-          const int ci = j * N + k;  // pair index of C_0j[k]; C_ij[k] is i*kb*N further
-#pragma unroll 4
-          for (int i = 0; i < q; ++i) a = slot_mac<S0, true>(a, cin.load(ci + i * kb * N), gk[i * REG]);
-          xk[j * REG] = a;
-        }
-      };
-      if (k == 0) grad_x(std::true_type{});
-      else grad_x(std::false_type{});
-    }
-    __syncthreads();
-
-    // Phase C: dx_j = irdFFT(dX_j)
-    for (int s0 = 0; s0 < nx; s0 += NG) {
-      const int s = s0 + grp;
-      const bool valid = s < nx;
-      const int tt = valid ? s / kb : 0, j = valid ? s - tt * kb : 0;
-      const bool act = valid && tt < nvalid;
-      float2* reg = valid ? xs + (size_t)s * REG : dummy;
-      const Out dst{dx + ((act ? tok0 + tt : 0) * kb + j) * (int64_t)N};
-      row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, tw);
-    }
-    __syncthreads();
-  }
-
-  if (!do_dc) return;
-  __syncthreads();
-  // fold this workgroup's partial sums into dc; workgroup b starts 64*b slots in, so
-  // that the workgroups, which all finish together, do not queue on the same addresses
-  const int shift = (int)(((unsigned)blockIdx.x * 64u) % (unsigned)qkn);
-  for (int e0 = tid; e0 < qkn; e0 += WG) {
-    int e = e0 + shift;
-    if (e >= qkn) e -= qkn;
-    const float2 v = acc[e];
-    const int k = e & (N - 1);
-    const int ij = e / N;
-    const int ii = ij / jb, jj = ij - ii * jb;
-    const int64_t d = ((int64_t)(i0 + ii) * kb + (j0 + jj)) * N + k;
-    unsafeAtomicAdd(dc + 2 * d, v.x);
-    unsafeAtomicAdd(dc + 2 * d + 1, v.y);
-  }
-}
-
-// Forward for square layers (q == kb == QB) with few blocks: a persistent workgroup
-// whose threads own fixed bins for the whole kernel and keep C_ij[k] for them in
-// registers (read from HBM once per workgroup rather than once per token).  With TB > 1
-// threads per bin the TB threads split the output blocks i into TJ groups and the
-// tokens of a tile into TS phases; with BT > 1 bins per thread a thread takes bins kt,
-// kt+WG, ...
-template <int LOGN, int QB, int WG>
-struct BcaSqFwd {
-  static constexpr int N = BcaPlan<LOGN>::N;
-  static constexpr int TB = WG >= N ? WG / N : 1;
-  static constexpr int BT = WG >= N ? 1 : N / WG;
-  static constexpr int TJ = TB % QB == 0 ? QB : (QB % TB == 0 ? TB : 1);  // output-block groups
-  static constexpr int TS = TB / TJ;                                        // token phases
-  static constexpr int IPT = QB / TJ;                                       // output blocks per thread
-  static constexpr int NSL = IPT * QB;
-};
-constexpr int kFwdSqWG = 512;
-
-template <int LOGN, class Elem, int QB, int WG = kFwdSqWG>
-__global__ void __launch_bounds__(WG) bca_forward_sq_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
-                                                                     Elem* y, int64_t tokens, int tt_per_tile,
-                                                                     int64_t ntiles, const float2* __restrict__ tw) {
-  using B = BcaPlan<LOGN>;
-  using S = BcaSqFwd<LOGN, QB, WG>;
-  using In = typename Acc<Elem>::In;
-  using Out = typename Acc<Elem>::Out;
-  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
-  constexpr int TB = S::TB, BT = S::BT, TJ = S::TJ, TS = S::TS, IPT = S::IPT, NSL = S::NSL;
-  static_assert(TJ * IPT == QB && TS * TJ == TB, "inconsistent split");
-  const int tid = threadIdx.x;
-  const int grp = tid / TPR, t = tid - grp * TPR;
-  const int u = TB > 1 ? tid / N : 0;
-  const int kt = TB > 1 ? tid - u * N : tid;
-  const int i0 = (u % TJ) * IPT;  // first output block of this thread
-  const int tu = u / TJ;          // token phase
-  const int TT = tt_per_tile;
-  // With one thread per bin, Y_i[k] overwrites X_i[k]: the thread has read every X_j[k]
-  // before it writes, and no other thread touches bin k, so a token needs QB regions.
-  constexpr bool INPLACE = TB == 1;
-  float2* const xs = bca_lds;                                         // TT*QB regions: X
-  float2* const ys = INPLACE ? xs : bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: Y
-  // spare region for row groups without a transform (allocated only when some exist)
-  float2* const dummy = bca_lds + (size_t)TT * (INPLACE ? 1 : 2) * QB * REG;
-
-  // slot (ii, j) is sl = ii*QB + j for output block i = i0 + ii
-  typename In::raw_t cr[BT][NSL];
-  {
-    const In cin{c};
-    static_for<BT>([&](auto wc) {
-      constexpr int w = decltype(wc)::value;
-      static_for<NSL>([&](auto sc) {
-        constexpr int sl = decltype(sc)::value, ii = sl / QB, j = sl % QB;
-        cr[w][sl] = cin.load_raw(((i0 + ii) * QB + j) * N + kt + w * WG);  // C_ij[k]
-      });
-    });
-  }
-
-  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    const int64_t tok0 = tile * TT;
-    const int nvalid = (int)(tokens - tok0 < TT ? tokens - tok0 : TT);
-
-    // Phase A: X_j = rdFFT(x_j)
-    const int nx = TT * QB;
-    for (int s0 = 0; s0 < nx; s0 += NG) {
-      const int s = s0 + grp;
-      const bool valid = s < nx;
-      const int tt = valid ? s / QB : 0, j = valid ? s - tt * QB : 0;
-      const bool act = valid && tt < nvalid;
-      float2* reg = valid ? xs + (size_t)s * REG : dummy;
-      const In src{x + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N};
-      row_forward<LOGN, true>(t, act, src, LdsSpectrum{reg}, reg, tw);
-    }
-    __syncthreads();
-
-    // Phase B: Y_i[k] = sum_j C_ij[k] . X_j[k]
-    static_for<BT>([&](auto wc) {
-      constexpr int w = decltype(wc)::value;
-      const int k = kt + w * WG;
-      const int pk = lds_pad(k);
-      auto block_sum = [&](auto s0c) {
-        constexpr bool S0 = decltype(s0c)::value;
-        for (int tt = tu; tt < nvalid; tt += TS) {
-          const float2* xk = xs + (size_t)tt * QB * REG + pk;
-          float2* yk = ys + ((size_t)tt * QB + i0) * REG + pk;
-          float2 X[QB];
-          static_for<QB>([&](auto jc) { X[decltype(jc)::value] = xk[decltype(jc)::value * REG]; });
-          static_for<IPT>([&](auto ic) {
-            constexpr int ii = decltype(ic)::value;
-            float2 a = make_float2(0.f, 0.f);
-            static_for<QB>([&](auto jc) {
-              constexpr int j = decltype(jc)::value;
-              a = slot_mac<S0, false>(a, In::widen(cr[w][ii * QB + j]), X[j]);
-            });
-            yk[ii * REG] = a;
-          });
-        }
-      };
-      if (k == 0) block_sum(std::true_type{});
-      else block_sum(std::false_type{});
-    });
-    __syncthreads();
-
-    // Phase C: y_i = irdFFT(Y_i)
-    for (int s0 = 0; s0 < nx; s0 += NG) {
-      const int s = s0 + grp;
-      const bool valid = s < nx;
-      const int tt = valid ? s / QB : 0, i = valid ? s - tt * QB : 0;
-      const bool act = valid && tt < nvalid;
-      float2* reg = valid ? ys + (size_t)s * REG : dummy;
-      const Out dst{y + ((act ? tok0 + tt : 0) * QB + i) * (int64_t)N};
-      row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, tw);
-    }
-    __syncthreads();
-  }
-}
-
-// Backward for square layers (q == kb == QB) with few blocks: every thread owns a fixed
-// set of (bin, input block) slots for the whole kernel, keeps C_ij[k] and its dC_ij[k]
-// partial sums for them in registers, and so touches LDS only to read X_j[k], G_i[k]
-// and to write dX_j[k].  With TB > 1 threads per bin (WG > N), the TB threads of a bin
-// split the input blocks j into TJ groups and the tokens of a tile into TS phases; with
-// BT > 1 bins per thread (N > WG) a thread takes bins kt, kt+WG, ...
-constexpr int gcd_int(int a, int b) { return b == 0 ? a : gcd_int(b, a % b); }
-
-template <int LOGN, int QB, int WG>
-struct BcaSq {
-  static constexpr int N = BcaPlan<LOGN>::N;
-  static constexpr int TB = WG >= N ? WG / N : 1;
-  static constexpr int BT = WG >= N ? 1 : N / WG;
-  static constexpr int TJ = gcd_int(TB, QB);  // input-block groups per bin
-  static constexpr int TS = TB / TJ;          // token phases per bin
-  static constexpr int JPT = QB / TJ;         // input blocks per thread
-  static constexpr int NSL = QB * JPT;        // (i, j) slots per bin per thread
-};
-
-template <int LOGN, class Elem, int QB, int WG = BcaPlan<LOGN>::BWD_WG>
-__global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const Elem* __restrict__ x, const Elem* __restrict__ c,
-                                                                      const Elem* gy, Elem* dx, float* __restrict__ dc,
-                                                                      int64_t tokens, int tt_per_tile, int64_t ntiles,
-                                                                      float2* stage, int64_t tile_f2, int chunk,
-                                                                      const float2* __restrict__ tw) {
-  using B = BcaPlan<LOGN>;
-  using S = BcaSq<LOGN, QB, WG>;
-  using In = typename Acc<Elem>::In;
-  using Out = typename Acc<Elem>::Out;
-  constexpr int N = B::N, TPR = B::TPR, NG = WG / TPR, REG = B::REGION;
-  constexpr int TB = S::TB, BT = S::BT, TJ = S::TJ, TS = S::TS, JPT = S::JPT, NSL = S::NSL;
-  const int tid = threadIdx.x;
-  const int grp = tid / TPR, t = tid - grp * TPR;
-  const int u = TB > 1 ? tid / N : 0;         // which of the bin's TB threads
-  const int kt = TB > 1 ? tid - u * N : tid;  // first bin of this thread
-  const int j0 = (u % TJ) * JPT;              // first input block of this thread
-  const int tu = u / TJ;                      // token phase
-  const int TT = tt_per_tile;
-  float2* const xs = bca_lds;                         // TT*QB regions: X, then dX
-  float2* const gs = bca_lds + (size_t)TT * QB * REG;  // TT*QB regions: G
-  // spare region for row groups without a transform (allocated only when some exist)
-  float2* const dummy = bca_lds + (size_t)TT * 2 * QB * REG;
-  if (stage != nullptr) {
-    // two-stage sum: this kernel never touches dc, and the reduce kernel that adds into it
-    // runs after it on the stream, so dc is zeroed here instead of by a launch of its own
-    for (int64_t e = (int64_t)blockIdx.x * WG + tid; e < 2 * (int64_t)QB * QB * N; e += (int64_t)gridDim.x * WG)
-      dc[e] = 0.f;
-  }
-
-  // slot (i, jj) is sl = i*JPT + jj, for input block j = j0 + jj.  C is kept in its
-  // storage form (half the registers for bf16) and widened where it is used.
-  typename In::raw_t cr[BT][NSL];
-  float2 dcr[BT][NSL];
-  {
-    const In cin{c};
-    static_for<BT>([&](auto wc) {
-      constexpr int w = decltype(wc)::value;
-      static_for<NSL>([&](auto sc) {
-        constexpr int sl = decltype(sc)::value, i = sl / JPT, jj = sl % JPT;
-        cr[w][sl] = cin.load_raw((i * QB + j0 + jj) * N + kt + w * WG);  // C_ij[k]
-        dcr[w][sl] = make_float2(0.f, 0.f);
-      });
-    });
-  }
-
-  for (int64_t tile = blockIdx.x; tile < ntiles; tile += gridDim.x) {
-    const int64_t tok0 = tile * TT;
-    const int nvalid = (int)(tokens - tok0 < TT ? tokens - tok0 : TT);
-
-    // Phase A: X_j = rdFFT(x_j), G_i = rdFFT(g_i)
-    const int nx = TT * QB, ns = 2 * TT * QB;
-    for (int s0 = 0; s0 < ns; s0 += NG) {
-      const int s = s0 + grp;
-      const bool valid = s < ns;
-      float2* reg = valid ? bca_lds + (size_t)s * REG : dummy;
-      const int sx = s < nx ? s : s - nx;
-      const int tt = sx / QB, j = sx - tt * QB;
-      const bool act = valid && tt < nvalid;
-      const Elem* base = s < nx ? x : gy;
-      const Elem* srcp = base + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N;
-      row_forward<LOGN, true>(t, act, In{srcp}, LdsSpectrum{reg}, reg, tw);
-    }
-    __syncthreads();
-
-    // Phase B: per (token, bin): dC_ij += conj(X_j) . G_i and dX_j = sum_i conj(C_ij) . G_i
-    static_for<BT>([&](auto wc) {
-      constexpr int w = decltype(wc)::value;
-      const int k = kt + w * WG;
-      const int pk = lds_pad(k);
-      auto contract = [&](auto s0c) {
-        constexpr bool S0 = decltype(s0c)::value;
-        for (int tt = tu; tt < nvalid; tt += TS) {
-          float2* xk = xs + ((size_t)tt * QB + j0) * REG + pk;
-          const float2* gk = gs + (size_t)tt * QB * REG + pk;
-          float2 X[JPT], G[QB];
-          static_for<JPT>([&](auto jc) { X[decltype(jc)::value] = xk[decltype(jc)::value * REG]; });
-          static_for<QB>([&](auto ic) { G[decltype(ic)::value] = gk[decltype(ic)::value * REG]; });
-          static_for<JPT>([&](auto jc) {
-            constexpr int jj = decltype(jc)::value;
-            float2 d = make_float2(0.f, 0.f);
-            static_for<QB>([&](auto ic) {
-              constexpr int i = decltype(ic)::value;
-              dcr[w][i * JPT + jj] = slot_mac<S0, true>(dcr[w][i * JPT + jj], X[jj], G[i]);
-              d = slot_mac<S0, true>(d, In::widen(cr[w][i * JPT + jj]), G[i]);
-            });
-            xk[jj * REG] = d;
-          });
-        }
-      };
-      if (k == 0) contract(std::true_type{});
-      else contract(std::false_type{});
-    });
-    __syncthreads();
-
-    // Phase C: dx_j = irdFFT(dX_j)
-    for (int s0 = 0; s0 < nx; s0 += NG) {
-      const int s = s0 + grp;
-      const bool valid = s < nx;
-      const int tt = valid ? s / QB : 0, j = valid ? s - tt * QB : 0;
-      const bool act = valid && tt < nvalid;
-      float2* reg = valid ? xs + (size_t)s * REG : dummy;
-      const Out dst{dx + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N};
-      row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, tw);
-    }
-    __syncthreads();
-  }
-
-  // Fold the partial sums into dc (slot e = (i*QB + j)*N + k, float2).  They are staged
-  // in LDS as [TS][QB*QB*N], the TS token phases summed, and the atomics issued from a
-  // rotated start: workgroup b begins 64*b slots in, so that the workgroups, which all
-  // finish together, do not queue on the same addresses.
-  constexpr int QKN = QB * QB * N;
-  float2* const part = bca_lds;
-  static_for<BT>([&](auto wc) {
-    constexpr int w = decltype(wc)::value;
-    static_for<NSL>([&](auto sc) {
-      constexpr int sl = decltype(sc)::value, i = sl / JPT, jj = sl % JPT;
-      part[(size_t)tu * QKN + (i * QB + j0 + jj) * N + kt + w * WG] = dcr[w][sl];
-    });
-  });
-  __syncthreads();
-  if (stage != nullptr) {
-    // Two-stage sum (dx is not gy): the partial sums go to the gy rows of this workgroup's
-    // first tiles, which it alone has read and nobody reads again, chunk c of them (chunk
-    // float2 each) to tile blockIdx.x + c*gridDim.x; bca_dc_reduce_kernel then adds the
-    // workgroups' partials into dc.
-    for (int e = tid; e < QKN; e += WG) {
-      float2 v = part[e];
-      static_for<TS - 1>([&](auto pc) { v = c_add(v, part[(size_t)(decltype(pc)::value + 1) * QKN + e]); });
-      const int ch = e / chunk;
-      stage[((int64_t)blockIdx.x + (int64_t)ch * gridDim.x) * tile_f2 + (e - ch * chunk)] = v;
-    }
-    return;
-  }
-  const int shift = (int)(((unsigned)blockIdx.x * 64u) % (unsigned)QKN);
-  for (int e0 = tid; e0 < QKN; e0 += WG) {
-    int e = e0 + shift;
-    if (e >= QKN) e -= QKN;
-    float2 v = part[e];
-    static_for<TS - 1>([&](auto pc) { v = c_add(v, part[(size_t)(decltype(pc)::value + 1) * QKN + e]); });
-    unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
-    unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
-  }
-}
 
 // Second stage of the two-stage dC sum: dc[e] += the partials of workgroups
 // b in [blockIdx.y*kReduceGroup, +kReduceGroup) (zeroed dc, one float32 atomic pair per
 // thread and group of workgroups).  Workgroup b's slot e lies at
 // stage[(b + c*groups)*tile_f2 + e - c*chunk], c = e / chunk.
-constexpr int kReduceGroup = 16;
-constexpr int64_t kStageMinAtomics = (int64_t)1 << 21;
 __global__ void __launch_bounds__(256) bca_dc_reduce_kernel(const float2* __restrict__ stage, float* __restrict__ dc,
                                                             int qkn, int chunk, int groups, int64_t tile_f2) {
   const int e = blockIdx.x * 256 + threadIdx.x;
@@ -568,273 +33,22 @@ __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
     p[i] = 0.f;
 }
 
-static hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t stream) {
+hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t stream) {
   const int blocks = (int)std::min<int64_t>((count + 255) / 256, 1024);
   hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, p, count);
   return hipGetLastError();
 }
 
-// ----------------------------------------------------------------------------------
-// host side
-
-static int region_bytes(int logn) {
-  static const int sizes[kMaxLogN + 1] = {
-      BcaPlan<0>::REGION,  BcaPlan<1>::REGION,  BcaPlan<2>::REGION,  BcaPlan<3>::REGION,
-      BcaPlan<4>::REGION,  BcaPlan<5>::REGION,  BcaPlan<6>::REGION,  BcaPlan<7>::REGION,
-      BcaPlan<8>::REGION,  BcaPlan<9>::REGION,  BcaPlan<10>::REGION, BcaPlan<11>::REGION,
-      BcaPlan<12>::REGION, 0, 0, 0};
-  return sizes[logn] * (int)sizeof(float2);
-}
-
-constexpr int kBcaMaxLogN = 12;        // p <= 8192
-constexpr int kLdsLimit = 160 * 1024;  // gfx950 LDS per workgroup
-constexpr int kFwdLdsTarget = 64 * 1024;  // forward: aim for two workgroups per CU
-
-template <int LOGN>
-static int fwd_wg() { return BcaPlan<LOGN>::FWD_WG; }
-static int bwd_wg(int logn) {
-  static const int wg[kBcaMaxLogN + 1] = {
-      BcaPlan<0>::BWD_WG, BcaPlan<1>::BWD_WG, BcaPlan<2>::BWD_WG,  BcaPlan<3>::BWD_WG,  BcaPlan<4>::BWD_WG,
-      BcaPlan<5>::BWD_WG, BcaPlan<6>::BWD_WG, BcaPlan<7>::BWD_WG,  BcaPlan<8>::BWD_WG,  BcaPlan<9>::BWD_WG,
-      BcaPlan<10>::BWD_WG, BcaPlan<11>::BWD_WG, BcaPlan<12>::BWD_WG};
-  return wg[logn];
-}
-static int tpr_of(int logn) {
-  static const int tpr[kBcaMaxLogN + 1] = {
-      BcaPlan<0>::TPR, BcaPlan<1>::TPR, BcaPlan<2>::TPR, BcaPlan<3>::TPR,  BcaPlan<4>::TPR,  BcaPlan<5>::TPR,
-      BcaPlan<6>::TPR, BcaPlan<7>::TPR, BcaPlan<8>::TPR, BcaPlan<9>::TPR, BcaPlan<10>::TPR, BcaPlan<11>::TPR,
-      BcaPlan<12>::TPR};
-  return tpr[logn];
-}
-
-// Tokens per tile: a tile's spectra plus one spare region must fit the LDS budget; the
-// tile is grown until every row group has a transform in the output phase.  0 when a
-// single token does not fit.
-static int tokens_per_tile(int logn, int kb, int q, int64_t tokens, int wg, int budget) {
-  const int rb = region_bytes(logn);
-  const int64_t per_tok = (int64_t)(kb + q) * rb;
-  if (per_tok + rb > budget) return 0;
-  const int ng = wg / tpr_of(logn);
-  int64_t tt = 1;
-  while ((tt + 1) * per_tok + rb <= budget && tt * kb < ng && tt < tokens && tt < 64) ++tt;
-  return (int)tt;
-}
-
-template <class K>
-static hipError_t set_lds_limit(K kernel) {
-  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                             kLdsLimit);
-}
-
-template <int LOGN, class Elem>
-static hipError_t fwd_impl(const BcaArgs& a, const float2* tw, hipStream_t stream) {
-  constexpr int WG = BcaPlan<LOGN>::FWD_WG;
-  const int TT = tokens_per_tile(LOGN, a.kb, a.q, a.tokens, WG, std::max(kFwdLdsTarget, 3 * region_bytes(LOGN)));
-  if (TT == 0) return hipErrorInvalidValue;
-  const size_t lds = (size_t)(TT * (a.kb + a.q) + 1) * region_bytes(LOGN);
-  static const hipError_t attr = set_lds_limit(bca_forward_kernel<LOGN, Elem>);
-  if (attr != hipSuccess) return attr;
-  // one workgroup per tile, in launches within the grid limit
-  const int64_t per_launch = (kMaxGridThreads / WG) * TT;
-  constexpr int64_t N = (int64_t)1 << LOGN;
-  for (int64_t t0 = 0; t0 < a.tokens; t0 += per_launch) {
-    const int64_t nt = std::min<int64_t>(per_launch, a.tokens - t0);
-    const int64_t tiles = (nt + TT - 1) / TT;
-    hipLaunchKernelGGL((bca_forward_kernel<LOGN, Elem>), dim3((unsigned)tiles), dim3(WG), lds, stream,
-                       static_cast<const Elem*>(a.x) + t0 * a.kb * N, static_cast<const Elem*>(a.c),
-                       static_cast<Elem*>(a.y) + t0 * a.q * N, nt, a.q, a.kb, TT, tw);
-    const hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-  }
-  return hipSuccess;
-}
-
-// LDS of the backward's dC partial sums: q*kb*p/2 pair slots of float2
-static int64_t dc_lds_bytes(int logn, int q, int kb) { return (int64_t)q * kb * ((int64_t)1 << logn) * 8; }
-
-template <int LOGN, class Elem>
-static hipError_t bwd_launch(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu, int i0, int ia,
-                             int j0, int jb, int mode) {
-  constexpr int WG = BcaPlan<LOGN>::BWD_WG;
-  const int64_t acc_bytes = (mode & kBwdDc) ? dc_lds_bytes(LOGN, ia, jb) : 0;
-  const int TT = tokens_per_tile(LOGN, jb, ia, a.tokens, WG, kLdsLimit - (int)acc_bytes);
-  if (TT == 0) return hipErrorInvalidValue;
-  const size_t lds = (size_t)(TT * (jb + ia) + 1) * region_bytes(LOGN) + (size_t)acc_bytes;
-  static const hipError_t attr = set_lds_limit(bca_backward_kernel<LOGN, Elem>);
-  if (attr != hipSuccess) return attr;
-  const int64_t tiles = (a.tokens + TT - 1) / TT;
-  // persistent workgroups, as many as fit at once: fewer workgroups, fewer dC partials
-  const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / WG));
-  const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
-  hipLaunchKernelGGL((bca_backward_kernel<LOGN, Elem>), dim3((unsigned)grid), dim3(WG), lds, stream,
-                     static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<const Elem*>(a.y),
-                     static_cast<Elem*>(a.dx), a.dc, a.tokens, a.q, a.kb, i0, ia, j0, jb, mode, TT, tiles, tw);
+hipError_t launch_dc_reduce(const float2* stage, float* dc, int qkn, int chunk, int groups, int64_t tile_f2,
+                            hipStream_t stream) {
+  const dim3 rgrid((unsigned)((qkn + 255) / 256), (unsigned)((groups + kReduceGroup - 1) / kReduceGroup));
+  hipLaunchKernelGGL(bca_dc_reduce_kernel, rgrid, dim3(256), 0, stream, stage, dc, qkn, chunk, groups, tile_f2);
   return hipGetLastError();
 }
 
-// Largest block ranges (ia output x jb input blocks) whose dC slots and spectra fit in LDS
-// together with one token (0 when even one block does not fit).
-static void dc_chunk(int logn, int q, int kb, int* ia, int* jb) {
-  const int64_t rb = region_bytes(logn), blk = dc_lds_bytes(logn, 1, 1);
-  int best_a = 0, best_b = 0;
-  for (int A = 1; A <= q; ++A) {
-    for (int Bj = kb; Bj >= 1; --Bj) {
-      if (A * Bj * blk + (int64_t)(A + Bj + 1) * rb <= kLdsLimit) {
-        const int64_t chunks = (int64_t)((q + A - 1) / A) * ((kb + Bj - 1) / Bj);
-        const int64_t best = best_a ? (int64_t)((q + best_a - 1) / best_a) * ((kb + best_b - 1) / best_b) : INT64_MAX;
-        if (chunks < best) best_a = A, best_b = Bj;
-        break;
-      }
-    }
-  }
-  *ia = best_a;
-  *jb = best_b;
-}
-
-template <int LOGN, class Elem>
-static hipError_t bwd_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
-  constexpr int WG = BcaPlan<LOGN>::BWD_WG;
-  const int64_t acc_bytes = dc_lds_bytes(LOGN, a.q, a.kb);
-  if (acc_bytes < kLdsLimit && tokens_per_tile(LOGN, a.kb, a.q, a.tokens, WG, kLdsLimit - (int)acc_bytes) > 0)
-    return bwd_launch<LOGN, Elem>(a, tw, stream, num_cu, 0, a.q, 0, a.kb, kBwdDx | kBwdDc);
-  // too many blocks for one LDS-resident dC: the dx path, then dC over block ranges
-  hipError_t e = bwd_launch<LOGN, Elem>(a, tw, stream, num_cu, 0, a.q, 0, a.kb, kBwdDx);
-  int ia = 0, jb = 0;
-  dc_chunk(LOGN, a.q, a.kb, &ia, &jb);
-  if (ia == 0) return hipErrorInvalidValue;
-  for (int i0 = 0; i0 < a.q && e == hipSuccess; i0 += ia)
-    for (int j0 = 0; j0 < a.kb && e == hipSuccess; j0 += jb)
-      e = bwd_launch<LOGN, Elem>(a, tw, stream, num_cu, i0, std::min(ia, a.q - i0), j0, std::min(jb, a.kb - j0),
-                                 kBwdDc);
-  return e;
-}
-
-// Square layers with few blocks: register-resident C and dC (bca_backward_sq_kernel)
-constexpr int kSqMaxBlocks = 4;  // q == kb <= 4
-constexpr int kSqMaxSlots = 16;  // C and dC values per thread: bins per thread * q * kb
-
-// Tokens per tile of the square-layer kernels: the largest TT (at most 64 and the token
-// count) whose TT*rpt spectra, plus a spare region when TT*QB transforms leave some of
-// the ng row groups idle, fit in `budget` bytes.  0 when one token does not fit.
-static int sq_tokens_per_tile(int logn, int rpt, int qb, int ng, int64_t tokens, int64_t budget, bool* spare) {
-  const int64_t rb = region_bytes(logn);
-  for (int tt = (int)std::min<int64_t>(64, std::max<int64_t>(tokens, 1)); tt >= 1; --tt) {
-    const bool sp = (tt * qb) % ng != 0;
-    if ((tt * rpt + (sp ? 1 : 0)) * rb <= budget) {
-      *spare = sp;
-      return tt;
-    }
-  }
-  return 0;
-}
-
-template <int LOGN, int QB>
-constexpr bool sq_fwd_fits() {
-  using S = BcaSqFwd<LOGN, QB, kFwdSqWG>;
-  return BcaPlan<LOGN>::TPR <= kFwdSqWG / 2 && S::BT * S::NSL <= kSqMaxSlots && S::TS <= 8;
-}
-
-template <int LOGN, class Elem, int QB>
-static hipError_t fwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
-  constexpr int WG = kFwdSqWG;
-  using S = BcaSqFwd<LOGN, QB, WG>;
-  constexpr int rpt = (S::TB == 1 ? 1 : 2) * QB;  // regions per token (Y over X when TB == 1)
-  constexpr int ng = WG / BcaPlan<LOGN>::TPR;
-  // two workgroups per CU, or one when a token's spectra need more than half the LDS
-  bool spare = false;
-  int TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit / 2, &spare);
-  if (TT == 0) TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit, &spare);
-  if (TT == 0) return hipErrorInvalidValue;
-  const size_t lds = (size_t)(TT * rpt + (spare ? 1 : 0)) * region_bytes(LOGN);
-  static const hipError_t attr = set_lds_limit(bca_forward_sq_kernel<LOGN, Elem, QB>);
-  if (attr != hipSuccess) return attr;
-  const int64_t tiles = (a.tokens + TT - 1) / TT;
-  const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / WG));
-  const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
-  hipLaunchKernelGGL((bca_forward_sq_kernel<LOGN, Elem, QB>), dim3((unsigned)grid), dim3(WG), lds, stream,
-                     static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<Elem*>(a.y), a.tokens,
-                     TT, tiles, tw);
-  return hipGetLastError();
-}
-
-template <int LOGN, int QB>
-constexpr bool sq_fits() {
-  using S = BcaSq<LOGN, QB, BcaPlan<LOGN>::BWD_WG>;
-  return S::BT * S::NSL <= kSqMaxSlots && S::TS <= 8;  // short rows: many threads per bin
-}
-
-template <int LOGN, class Elem, int QB>
-static hipError_t bwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
-  constexpr int WG = BcaPlan<LOGN>::BWD_WG;
-  using S = BcaSq<LOGN, QB, WG>;
-  bool spare = false;
-  const int TT = sq_tokens_per_tile(LOGN, 2 * QB, QB, WG / BcaPlan<LOGN>::TPR, a.tokens, kLdsLimit, &spare);
-  if (TT == 0) return hipErrorInvalidValue;
-  const size_t spectra = (size_t)(TT * 2 * QB + (spare ? 1 : 0)) * region_bytes(LOGN);
-  const size_t part = (size_t)S::TS * QB * QB * S::N * sizeof(float2);  // [TS][QB*QB*N]
-  const size_t lds = std::max(spectra, part);
-  if (lds > (size_t)kLdsLimit) return hipErrorInvalidValue;
-  static const hipError_t attr = set_lds_limit(bca_backward_sq_kernel<LOGN, Elem, QB>);
-  if (attr != hipSuccess) return attr;
-  const int64_t tiles = (a.tokens + TT - 1) / TT;
-  const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / WG));
-  const int64_t grid = std::min<int64_t>(tiles, (int64_t)num_cu * per_cu);
-  // Two-stage dC sum when dx has its own buffer: each workgroup's partial sums (QKN float2)
-  // fit in the gy rows of its first `chunks` tiles, all of them full tiles
-  constexpr int QKN = QB * QB * S::N;
-  const int64_t tile_bytes = (int64_t)TT * QB * S::N * (int64_t)sizeof(Elem);
-  const int64_t tile_f2 = tile_bytes / (int64_t)sizeof(float2);
-  const int chunk = (int)std::max<int64_t>(1, std::min<int64_t>(QKN, tile_f2));
-  const int64_t chunks = (QKN + chunk - 1) / chunk;
-  // (worth a second launch only when the atomics it replaces are many: 4.2M float32 atomics
-  // for the 4096-wide layer took ~24 us, 0.6M for the 768-wide one less than the launch)
-  const bool staged = a.dx != a.y && tile_bytes % (int64_t)sizeof(float2) == 0 && chunks * grid <= a.tokens / TT &&
-                      2 * (int64_t)QKN * grid >= kStageMinAtomics;
-  float2* const stage = staged ? static_cast<float2*>(a.y) : nullptr;
-  if (!staged) {  // the kernel's atomics add into dc
-    const hipError_t ez = launch_fill_zero(a.dc, 2 * (int64_t)QKN, stream);
-    if (ez != hipSuccess) return ez;
-  }
-  hipLaunchKernelGGL((bca_backward_sq_kernel<LOGN, Elem, QB>), dim3((unsigned)grid), dim3(WG), lds, stream,
-                     static_cast<const Elem*>(a.x), static_cast<const Elem*>(a.c), static_cast<const Elem*>(a.y),
-                     static_cast<Elem*>(a.dx), a.dc, a.tokens, TT, tiles, stage, tile_f2, chunk, tw);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !staged) return e;
-  const dim3 rgrid((unsigned)((QKN + 255) / 256), (unsigned)((grid + kReduceGroup - 1) / kReduceGroup));
-  hipLaunchKernelGGL(bca_dc_reduce_kernel, rgrid, dim3(256), 0, stream, stage, a.dc, QKN, chunk, (int)grid, tile_f2);
-  return hipGetLastError();
-}
-
-using BcaFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t);
-using BcaBwdFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t, int);
-
-template <int LOGN, class Elem, int QB>
-static constexpr BcaBwdFn sq_fwd_entry() {
-  if constexpr (sq_fwd_fits<LOGN, QB>()) return &fwd_sq_impl<LOGN, Elem, QB>;
-  else return nullptr;
-}
-template <int QB, int... L>
-static std::array<BcaBwdFn, sizeof...(L)> sq_fwd_table(bool bf16, std::integer_sequence<int, L...>) {
-  return {(bf16 ? sq_fwd_entry<L, uint32_t, QB>() : sq_fwd_entry<L, float2, QB>())...};
-}
-
-template <int LOGN, class Elem, int QB>
-static constexpr BcaBwdFn sq_entry() {
-  if constexpr (sq_fits<LOGN, QB>()) return &bwd_sq_impl<LOGN, Elem, QB>;
-  else return nullptr;
-}
-template <int QB, int... L>
-static std::array<BcaBwdFn, sizeof...(L)> sq_table(bool bf16, std::integer_sequence<int, L...>) {
-  return {(bf16 ? sq_entry<L, uint32_t, QB>() : sq_entry<L, float2, QB>())...};
-}
-
-template <int... L>
-static std::array<BcaFn, sizeof...(L)> fwd_table(bool bf16, std::integer_sequence<int, L...>) {
-  return {(bf16 ? &fwd_impl<L, uint32_t> : &fwd_impl<L, float2>)...};
-}
-template <int... L>
-static std::array<BcaBwdFn, sizeof...(L)> bwd_table(bool bf16, std::integer_sequence<int, L...>) {
-  return {(bf16 ? &bwd_impl<L, uint32_t> : &bwd_impl<L, float2>)...};
+static const BcaStoreTables& store_tables(int storage) {
+  static const BcaStoreTables t[kStorages] = {bca_tables_f32(), bca_tables_bf16(), bca_tables_f16()};
+  return t[storage];
 }
 
 bool bca_shape_supported(int logp, int q, int kb, bool backward) {
@@ -851,34 +65,26 @@ bool bca_shape_supported(int logp, int q, int kb, bool backward) {
 }
 
 hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
-  static const auto seq = std::make_integer_sequence<int, kBcaMaxLogN + 1>{};
-  static const std::array<BcaFn, kBcaMaxLogN + 1> tab[2] = {fwd_table(false, seq), fwd_table(true, seq)};
-  static const std::array<BcaBwdFn, kBcaMaxLogN + 1> sq[2][kSqMaxBlocks] = {
-      {sq_fwd_table<1>(false, seq), sq_fwd_table<2>(false, seq), sq_fwd_table<3>(false, seq),
-       sq_fwd_table<4>(false, seq)},
-      {sq_fwd_table<1>(true, seq), sq_fwd_table<2>(true, seq), sq_fwd_table<3>(true, seq),
-       sq_fwd_table<4>(true, seq)}};
+  if (a.storage < 0 || a.storage >= kStorages) return hipErrorInvalidValue;
+  const BcaStoreTables& t = store_tables(a.storage);
   if (a.logp - 1 > kBcaMaxLogN) return launch_bca_multipass(a, false, tw, stream, num_cu);
   if (a.logp - 1 == kCirculantLogN && a.q == 1 && a.kb == 1) return launch_bca_circulant(a, tw, stream);
   if (a.q == a.kb && a.q <= kSqMaxBlocks) {
-    const BcaBwdFn fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
+    const BcaBwdFn fn = t.sq_fwd[a.q - 1][a.logp - 1];
     if (fn != nullptr) return fn(a, tw, stream, num_cu);
   }
-  return tab[a.bf16 ? 1 : 0][a.logp - 1](a, tw, stream);
+  return t.fwd[a.logp - 1](a, tw, stream);
 }
 
 hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
-  static const auto seq = std::make_integer_sequence<int, kBcaMaxLogN + 1>{};
-  static const std::array<BcaBwdFn, kBcaMaxLogN + 1> tab[2] = {bwd_table(false, seq), bwd_table(true, seq)};
+  if (a.storage < 0 || a.storage >= kStorages) return hipErrorInvalidValue;
+  const BcaStoreTables& t = store_tables(a.storage);
   const int64_t slots = (int64_t)a.q * a.kb * ((int64_t)1 << (a.logp - 1)) * 2;
-  static const std::array<BcaBwdFn, kBcaMaxLogN + 1> sq[2][kSqMaxBlocks] = {
-      {sq_table<1>(false, seq), sq_table<2>(false, seq), sq_table<3>(false, seq), sq_table<4>(false, seq)},
-      {sq_table<1>(true, seq), sq_table<2>(true, seq), sq_table<3>(true, seq), sq_table<4>(true, seq)}};
   // the square-layer kernels zero dc themselves (in the kernel when the dC sum is staged);
   // every other path finds it zeroed
   BcaBwdFn sq_fn = nullptr;
   if (a.tokens > 0 && a.logp - 1 <= kBcaMaxLogN && a.q == a.kb && a.q <= kSqMaxBlocks)
-    sq_fn = sq[a.bf16 ? 1 : 0][a.q - 1][a.logp - 1];
+    sq_fn = t.sq_bwd[a.q - 1][a.logp - 1];
   hipError_t e = hipSuccess;
   if (sq_fn == nullptr) {
     e = launch_fill_zero(a.dc, slots, stream);
@@ -889,7 +95,7 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
   } else if (a.logp - 1 > kBcaMaxLogN) {
     e = launch_bca_multipass(a, true, tw, stream, num_cu);
   } else {
-    e = tab[a.bf16 ? 1 : 0][a.logp - 1](a, tw, stream, num_cu);
+    e = t.bwd[a.logp - 1](a, tw, stream, num_cu);
   }
   if (e != hipSuccess) return e;
   // dc holds sum_t conj(X) . G as packed spectra; transform them in place to time domain

@@ -38,37 +38,13 @@ __device__ __forceinline__ float2 slot_mul(int m, float2 a, float2 w) {
   return m == 0 ? re : c_mul<CONJ>(a, w);
 }
 
-__device__ __forceinline__ float2 widen_slot(float2 v) { return v; }
-__device__ __forceinline__ float2 widen_slot(uint32_t v) { return bf16x2_to_f32(v); }
-template <class Elem>
-__device__ __forceinline__ Elem narrow_slot(float2 v);
-template <>
-__device__ __forceinline__ float2 narrow_slot<float2>(float2 v) {
-  return v;
-}
-template <>
-__device__ __forceinline__ uint32_t narrow_slot<uint32_t>(float2 v) {
-  return f32_to_bf16x2(v);
-}
+// the pair type a storage struct keeps in memory
+template <class St>
+using ElemOf = typename St::Elem;
 
-template <class Elem>
-struct StorageOf;
-template <>
-struct StorageOf<float2> {
-  using Acc = GlobalF32;
-  using Const = ConstF32;
-  static constexpr bool kHalf = false;
-};
-template <>
-struct StorageOf<uint32_t> {
-  using Acc = GlobalBF16;
-  using Const = ConstBF16;
-  static constexpr bool kHalf = true;
-};
-
-template <int LOGN, class Elem>
+template <int LOGN, class St>
 constexpr int mp_chunks() {
-  return StorageOf<Elem>::kHalf ? kChunksBf16[LOGN] : kChunks[LOGN];
+  return St::kHalf ? kChunksBf16[LOGN] : kChunks[LOGN];
 }
 
 // Load accessor that returns the product of a stored spectrum slot with the matching
@@ -85,68 +61,68 @@ struct MulLoad {
 
 // Forward transform of rows r < rows of src into dst row (r / gin) * gout + r % gin
 // (src == dst with gin == gout is the in-place transform).
-template <int LOGN, class Elem>
-__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
-    mp_forward_kernel(const Elem* src, Elem* dst, int64_t rows, int gin, int gout, const float2* __restrict__ tw) {
-  constexpr int CH = mp_chunks<LOGN, Elem>();
+template <int LOGN, class St>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, St>()>::WG))
+    mp_forward_kernel(const ElemOf<St>* src, ElemOf<St>* dst, int64_t rows, int gin, int gout, const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, St>();
   using P = RowPlan<LOGN, CH>;
   static_assert(P::RW == 1, "one row per workgroup");
-  using S = StorageOf<Elem>;
+  using S = St;
   __shared__ float2 lds[P::LDS_F2];
   const int t = threadIdx.x;
   const int64_t row = blockIdx.x;
   if (row >= rows) return;  // whole workgroup: no barrier is skipped by part of it
   const int64_t out_row = (row / gin) * gout + row % gin;
-  const typename S::Const in{src + row * (int64_t)P::N};
-  const typename S::Acc out{dst + out_row * (int64_t)P::N};
-  row_forward<LOGN, false, typename S::Const, typename S::Acc, CH>(t, true, in, out, lds, tw);
+  const typename S::In in{src + row * (int64_t)P::N};
+  const typename S::Out out{dst + out_row * (int64_t)P::N};
+  row_forward<LOGN, false, typename S::In, typename S::Out, CH>(t, true, in, out, lds, tw);
 }
 
 // dst row r = IFFT(spec . src row r), or IFFT(conj(spec) . src row r) when CONJ: the
 // last step of a single-block layer's forward (in place) and of its dx.  Every load of
 // a row precedes its first store, so src may be dst.
-template <int LOGN, class Elem, bool CONJ>
-__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
-    mp_inverse_mul_kernel(const Elem* src, Elem* dst, const Elem* spec, int64_t rows, const float2* __restrict__ tw) {
-  constexpr int CH = mp_chunks<LOGN, Elem>();
+template <int LOGN, class St, bool CONJ>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, St>()>::WG))
+    mp_inverse_mul_kernel(const ElemOf<St>* src, ElemOf<St>* dst, const ElemOf<St>* spec, int64_t rows, const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, St>();
   using P = RowPlan<LOGN, CH>;
   static_assert(P::RW == 1, "one row per workgroup");
-  using S = StorageOf<Elem>;
+  using S = St;
   __shared__ float2 lds[P::LDS_F2];
   const int t = threadIdx.x;
   const int64_t row = blockIdx.x;
   if (row >= rows) return;
-  const MulLoad<typename S::Const, typename S::Const, CONJ> in{typename S::Const{src + row * (int64_t)P::N},
-                                                              typename S::Const{spec}};
-  const typename S::Acc out{dst + row * (int64_t)P::N};
-  row_inverse<LOGN, false, decltype(in), typename S::Acc, CH>(t, true, in, out, lds, tw);
+  const MulLoad<typename S::In, typename S::In, CONJ> in{typename S::In{src + row * (int64_t)P::N},
+                                                              typename S::In{spec}};
+  const typename S::Out out{dst + row * (int64_t)P::N};
+  row_inverse<LOGN, false, decltype(in), typename S::Out, CH>(t, true, in, out, lds, tw);
 }
 
 // y row r = IFFT(spec . FFT(x row r)) for one block spectrum spec (a single circulant,
 // q == kb == 1): the forward post-pass leaves thread t the slots the inverse pre-pass of
 // the same thread reads (RegSpectrum), so the row goes from x to y in one pass over HBM.
 // Every load of a row precedes its first store, so x may be y.
-template <int LOGN, class Elem>
-__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
-    mp_circulant_kernel(const Elem* x, Elem* y, const Elem* spec, int64_t rows, const float2* __restrict__ tw) {
-  constexpr int CH = mp_chunks<LOGN, Elem>();
+template <int LOGN, class St>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, St>()>::WG))
+    mp_circulant_kernel(const ElemOf<St>* x, ElemOf<St>* y, const ElemOf<St>* spec, int64_t rows, const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, St>();
   using P = RowPlan<LOGN, CH>;
   static_assert(P::RW == 1, "one row per workgroup");
   constexpr int N = P::N, E = P::E, TPR = P::TPR;
   constexpr int R0 = radix(LOGN, 0), BPT0 = E / R0;
-  using S = StorageOf<Elem>;
+  using S = St;
   __shared__ float2 lds[P::LDS_F2];
   const int t = threadIdx.x;
   const int64_t row = blockIdx.x;
   if (row >= rows) return;
-  typename S::Const::raw_t raw[E];
-  load_forward<LOGN>(t, typename S::Const{x + row * (int64_t)N}, raw);
+  typename S::In::raw_t raw[E];
+  load_forward<LOGN>(t, typename S::In{x + row * (int64_t)N}, raw);
   float2 lo[E / 2], hi[E / 2];
   // DST_IN_LDS: a barrier after the post-pass's last LDS read, before the inverse's writes
-  row_forward_loaded<LOGN, true, typename S::Const, RegSpectrum, CH>(t, true, raw, RegSpectrum{lo, hi}, lds, tw);
+  row_forward_loaded<LOGN, true, typename S::In, RegSpectrum, CH>(t, true, raw, RegSpectrum{lo, hi}, lds, tw);
   // Y . C on slot k_j = t + j*TPR and its partner; slot 0 (thread 0, j = 0) holds the two
   // real bins Y_0, Y_{n/2}, and its partner is the complex bin N/2
-  const typename S::Const cin{spec};
+  const typename S::In cin{spec};
   static_for<E / 2>([&](auto jc) {
     constexpr int j = decltype(jc)::value;
     const int k = t + j * TPR;
@@ -171,38 +147,38 @@ __global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, Elem>()>::WG))
       inv[b * R0 + R0 / 2 + r] = hi[b + BPT0 * r];
     });
   });
-  row_inverse_loaded<LOGN, false, RegSource, typename S::Acc, CH>(t, true, inv, typename S::Acc{y + row * (int64_t)N},
+  row_inverse_loaded<LOGN, false, RegSource, typename S::Out, CH>(t, true, inv, typename S::Out{y + row * (int64_t)N},
                                                                   lds, tw);
 }
 
 // Per bin, in place in y: Y_ti = sum_j C_ij X_tj, with X_tj in y's segment j (kb <= q).
 // One thread owns slot m of one token across all segments, so it reads every X_tj[m]
 // before it writes any Y_ti[m].
-template <class Elem>
-__global__ void __launch_bounds__(256) mp_fwd_product_kernel(Elem* y, const Elem* c, int64_t tokens, int q, int kb,
+template <class St>
+__global__ void __launch_bounds__(256) mp_fwd_product_kernel(ElemOf<St>* y, const ElemOf<St>* c, int64_t tokens, int q, int kb,
                                                              int nslots, int xblocks) {
   const int64_t b = blockIdx.x;
   const int64_t tok = b / xblocks;
   const int m = (int)(b - tok * xblocks) * 256 + threadIdx.x;
   if (tok >= tokens || m >= nslots) return;
-  Elem* yt = y + tok * (int64_t)q * nslots;
+  ElemOf<St>* yt = y + tok * (int64_t)q * nslots;
   float2 xv[kMpMaxKb];
 #pragma unroll
   for (int j = 0; j < kMpMaxKb; ++j)
-    if (j < kb) xv[j] = widen_slot(yt[(int64_t)j * nslots + m]);
+    if (j < kb) xv[j] = St::Out::widen(yt[(int64_t)j * nslots + m]);
   for (int i = 0; i < q; ++i) {
-    const Elem* ci = c + (int64_t)i * kb * nslots + m;
+    const ElemOf<St>* ci = c + (int64_t)i * kb * nslots + m;
     float2 acc = make_float2(0.f, 0.f);
 #pragma unroll
     for (int j = 0; j < kMpMaxKb; ++j)
-      if (j < kb) acc = c_add(acc, slot_mul<false>(m, xv[j], widen_slot(ci[(int64_t)j * nslots])));
-    yt[(int64_t)i * nslots + m] = narrow_slot<Elem>(acc);
+      if (j < kb) acc = c_add(acc, slot_mul<false>(m, xv[j], St::Out::widen(ci[(int64_t)j * nslots])));
+    yt[(int64_t)i * nslots + m] = St::Out::narrow(acc);
   }
 }
 
 // Per bin: dX_tj = sum_i conj(C_ij) G_ti into dx (G in gy).  Thread: slot m of (t, j).
-template <class Elem>
-__global__ void __launch_bounds__(256) mp_dx_product_kernel(const Elem* g, const Elem* c, Elem* dx, int64_t tokens,
+template <class St>
+__global__ void __launch_bounds__(256) mp_dx_product_kernel(const ElemOf<St>* g, const ElemOf<St>* c, ElemOf<St>* dx, int64_t tokens,
                                                             int q, int kb, int nslots, int xblocks) {
   const int64_t b = blockIdx.x;
   const int64_t row = b / xblocks;  // t * kb + j
@@ -210,17 +186,17 @@ __global__ void __launch_bounds__(256) mp_dx_product_kernel(const Elem* g, const
   if (row >= tokens * kb || m >= nslots) return;
   const int64_t tok = row / kb;
   const int j = (int)(row - tok * kb);
-  const Elem* gt = g + tok * (int64_t)q * nslots + m;
-  const Elem* cj = c + (int64_t)j * nslots + m;
+  const ElemOf<St>* gt = g + tok * (int64_t)q * nslots + m;
+  const ElemOf<St>* cj = c + (int64_t)j * nslots + m;
   float2 acc = make_float2(0.f, 0.f);
   for (int i = 0; i < q; ++i)
-    acc = c_add(acc, slot_mul<true>(m, widen_slot(gt[(int64_t)i * nslots]), widen_slot(cj[(int64_t)i * kb * nslots])));
-  dx[row * nslots + m] = narrow_slot<Elem>(acc);
+    acc = c_add(acc, slot_mul<true>(m, St::Out::widen(gt[(int64_t)i * nslots]), St::Out::widen(cj[(int64_t)i * kb * nslots])));
+  dx[row * nslots + m] = St::Out::narrow(acc);
 }
 
 // dC_ij[m] += sum_{t in chunk} conj(X_tj[m]) G_ti[m]; grid (slot blocks, q*kb, chunks).
-template <class Elem>
-__global__ void __launch_bounds__(256) mp_dc_kernel(const Elem* xs, const Elem* g, float* dc, int64_t tokens, int q,
+template <class St>
+__global__ void __launch_bounds__(256) mp_dc_kernel(const ElemOf<St>* xs, const ElemOf<St>* g, float* dc, int64_t tokens, int q,
                                                     int kb, int nslots, int64_t tch) {
   const int m = blockIdx.x * 256 + threadIdx.x;
   if (m >= nslots) return;
@@ -228,13 +204,13 @@ __global__ void __launch_bounds__(256) mp_dc_kernel(const Elem* xs, const Elem* 
   const int i = pair / kb, j = pair - (pair / kb) * kb;
   const int64_t t0 = (int64_t)blockIdx.z * tch;
   const int64_t t1 = t0 + tch < tokens ? t0 + tch : tokens;
-  const Elem* xp = xs + (t0 * kb + j) * (int64_t)nslots + m;
-  const Elem* gp = g + (t0 * q + i) * (int64_t)nslots + m;
+  const ElemOf<St>* xp = xs + (t0 * kb + j) * (int64_t)nslots + m;
+  const ElemOf<St>* gp = g + (t0 * q + i) * (int64_t)nslots + m;
   const int64_t xstep = (int64_t)kb * nslots, gstep = (int64_t)q * nslots;
   float2 acc = make_float2(0.f, 0.f);
 #pragma unroll 8
   for (int64_t tok = t0; tok < t1; ++tok, xp += xstep, gp += gstep)
-    acc = c_add(acc, slot_mul<true>(m, widen_slot(*gp), widen_slot(*xp)));
+    acc = c_add(acc, slot_mul<true>(m, St::Out::widen(*gp), St::Out::widen(*xp)));
   float* d = dc + 2 * ((int64_t)pair * nslots + m);
   unsafeAtomicAdd(d, acc.x);
   unsafeAtomicAdd(d + 1, acc.y);
@@ -243,18 +219,18 @@ __global__ void __launch_bounds__(256) mp_dc_kernel(const Elem* xs, const Elem* 
 // workgroups per launch: a dimension of the grid holds fewer than 2^32 work-items
 constexpr int64_t kMaxGrid256 = kMaxGridThreads / 256;
 
-template <int LOGN, class Elem>
+template <int LOGN, class St>
 hipError_t forward_rows(const void* src, void* dst, int64_t rows, int gin, int gout, const float2* tw,
                         hipStream_t stream) {
   constexpr int N = 1 << LOGN;
-  using P = RowPlan<LOGN, mp_chunks<LOGN, Elem>()>;
-  const Elem* s = static_cast<const Elem*>(src);
-  Elem* d = static_cast<Elem*>(dst);
+  using P = RowPlan<LOGN, mp_chunks<LOGN, St>()>;
+  const ElemOf<St>* s = static_cast<const ElemOf<St>*>(src);
+  ElemOf<St>* d = static_cast<ElemOf<St>*>(dst);
   for (int64_t r0 = 0; r0 < rows;) {
     const int64_t nr = std::min<int64_t>(rows - r0, kMaxGridThreads / P::WG);
     // chunks start at a multiple of gin so the destination mapping restarts cleanly
     const int64_t step = nr == rows - r0 ? nr : (nr / gin) * gin;
-    hipLaunchKernelGGL((mp_forward_kernel<LOGN, Elem>), dim3((unsigned)step), dim3(P::WG), 0, stream,
+    hipLaunchKernelGGL((mp_forward_kernel<LOGN, St>), dim3((unsigned)step), dim3(P::WG), 0, stream,
                        s + r0 * (int64_t)N, d + (r0 / gin) * gout * (int64_t)N, step, gin, gout, tw);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -263,16 +239,16 @@ hipError_t forward_rows(const void* src, void* dst, int64_t rows, int gin, int g
   return hipSuccess;
 }
 
-template <int LOGN, class Elem, bool CONJ>
+template <int LOGN, class St, bool CONJ>
 hipError_t inverse_mul_rows(const void* src, void* dst, const void* spec, int64_t rows, const float2* tw,
                             hipStream_t stream) {
   constexpr int N = 1 << LOGN;
-  using P = RowPlan<LOGN, mp_chunks<LOGN, Elem>()>;
+  using P = RowPlan<LOGN, mp_chunks<LOGN, St>()>;
   for (int64_t r0 = 0; r0 < rows;) {
     const int64_t nr = std::min<int64_t>(rows - r0, kMaxGridThreads / P::WG);
-    hipLaunchKernelGGL((mp_inverse_mul_kernel<LOGN, Elem, CONJ>), dim3((unsigned)nr), dim3(P::WG), 0, stream,
-                       static_cast<const Elem*>(src) + r0 * (int64_t)N, static_cast<Elem*>(dst) + r0 * (int64_t)N,
-                       static_cast<const Elem*>(spec), nr, tw);
+    hipLaunchKernelGGL((mp_inverse_mul_kernel<LOGN, St, CONJ>), dim3((unsigned)nr), dim3(P::WG), 0, stream,
+                       static_cast<const ElemOf<St>*>(src) + r0 * (int64_t)N, static_cast<ElemOf<St>*>(dst) + r0 * (int64_t)N,
+                       static_cast<const ElemOf<St>*>(spec), nr, tw);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     r0 += nr;
@@ -294,16 +270,16 @@ hipError_t per_row_slots(int64_t nrows, int per, F launch) {
   return hipSuccess;
 }
 
-template <int LOGN, class Elem>
+template <int LOGN, class St>
 hipError_t circulant_rows(const void* x, void* y, const void* spec, int64_t rows, const float2* tw,
                           hipStream_t stream) {
   constexpr int N = 1 << LOGN;
-  using P = RowPlan<LOGN, mp_chunks<LOGN, Elem>()>;
+  using P = RowPlan<LOGN, mp_chunks<LOGN, St>()>;
   for (int64_t r0 = 0; r0 < rows;) {
     const int64_t nr = std::min<int64_t>(rows - r0, kMaxGridThreads / P::WG);
-    hipLaunchKernelGGL((mp_circulant_kernel<LOGN, Elem>), dim3((unsigned)nr), dim3(P::WG), 0, stream,
-                       static_cast<const Elem*>(x) + r0 * (int64_t)N, static_cast<Elem*>(y) + r0 * (int64_t)N,
-                       static_cast<const Elem*>(spec), nr, tw);
+    hipLaunchKernelGGL((mp_circulant_kernel<LOGN, St>), dim3((unsigned)nr), dim3(P::WG), 0, stream,
+                       static_cast<const ElemOf<St>*>(x) + r0 * (int64_t)N, static_cast<ElemOf<St>*>(y) + r0 * (int64_t)N,
+                       static_cast<const ElemOf<St>*>(spec), nr, tw);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     r0 += nr;
@@ -311,39 +287,39 @@ hipError_t circulant_rows(const void* x, void* y, const void* spec, int64_t rows
   return hipSuccess;
 }
 
-template <int LOGN, class Elem>
+template <int LOGN, class St>
 hipError_t mp_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
   constexpr int N = 1 << LOGN;
-  const int storage = StorageOf<Elem>::kHalf ? kStorageBF16 : kStorageF32;
+  constexpr int storage = St::kId;
   const int64_t xrows = a.tokens * a.kb;
   // single circulant: one fused row pass where the registers hold both spectra (p <= 32768);
   // for p = 65536 the row already fills the registers, so forward, then inverse with the
   // product taken as it loads
   if constexpr (LOGN < kMpMaxLogN) {
-    if (a.q == 1 && a.kb == 1) return circulant_rows<LOGN, Elem>(a.x, a.y, a.c, xrows, tw, stream);
+    if (a.q == 1 && a.kb == 1) return circulant_rows<LOGN, St>(a.x, a.y, a.c, xrows, tw, stream);
   }
-  hipError_t e = forward_rows<LOGN, Elem>(a.x, a.y, xrows, a.kb, a.q, tw, stream);
+  hipError_t e = forward_rows<LOGN, St>(a.x, a.y, xrows, a.kb, a.q, tw, stream);
   if (e != hipSuccess) return e;
-  if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, Elem, false>(a.y, a.y, a.c, xrows, tw, stream);
+  if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, St, false>(a.y, a.y, a.c, xrows, tw, stream);
   const int xblocks = (N + 255) / 256;
-  Elem* y = static_cast<Elem*>(a.y);
+  ElemOf<St>* y = static_cast<ElemOf<St>*>(a.y);
   e = per_row_slots(a.tokens, xblocks, [&](int64_t r0, int64_t nr, unsigned blocks) {
-    hipLaunchKernelGGL(mp_fwd_product_kernel<Elem>, dim3(blocks), dim3(256), 0, stream, y + r0 * (int64_t)a.q * N,
-                       static_cast<const Elem*>(a.c), nr, a.q, a.kb, N, xblocks);
+    hipLaunchKernelGGL(mp_fwd_product_kernel<St>, dim3(blocks), dim3(256), 0, stream, y + r0 * (int64_t)a.q * N,
+                       static_cast<const ElemOf<St>*>(a.c), nr, a.q, a.kb, N, xblocks);
   });
   if (e != hipSuccess) return e;
   return launch_rdfft_rows(a.y, a.tokens * a.q, LOGN, storage, true, tw, stream, num_cu);
 }
 
-template <int LOGN, class Elem>
+template <int LOGN, class St>
 hipError_t mp_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
   constexpr int N = 1 << LOGN;
-  const int storage = StorageOf<Elem>::kHalf ? kStorageBF16 : kStorageF32;
+  constexpr int storage = St::kId;
   const int64_t grows = a.tokens * a.q, xrows = a.tokens * a.kb;
   // G = FFT(g) in place; X = FFT(x) into dx
   hipError_t e = launch_rdfft_rows(a.y, grows, LOGN, storage, false, tw, stream, num_cu);
   if (e != hipSuccess) return e;
-  e = forward_rows<LOGN, Elem>(a.x, a.dx, xrows, 1, 1, tw, stream);
+  e = forward_rows<LOGN, St>(a.x, a.dx, xrows, 1, 1, tw, stream);
   if (e != hipSuccess) return e;
   // dC: slot blocks x pairs x token chunks, about 2048 workgroups in all (q * kb <= 65535)
   const int xblocks = (N + 255) / 256;
@@ -352,17 +328,17 @@ hipError_t mp_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, i
   chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, a.tokens / 16));
   int64_t tch = std::max<int64_t>((a.tokens + chunks - 1) / chunks, (a.tokens + 65534) / 65535);
   chunks = (a.tokens + tch - 1) / tch;
-  hipLaunchKernelGGL(mp_dc_kernel<Elem>, dim3(xblocks, pairs, (unsigned)chunks), dim3(256), 0, stream,
-                     static_cast<const Elem*>(a.dx), static_cast<const Elem*>(a.y), a.dc, a.tokens, a.q, a.kb, N,
+  hipLaunchKernelGGL(mp_dc_kernel<St>, dim3(xblocks, pairs, (unsigned)chunks), dim3(256), 0, stream,
+                     static_cast<const ElemOf<St>*>(a.dx), static_cast<const ElemOf<St>*>(a.y), a.dc, a.tokens, a.q, a.kb, N,
                      tch);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, Elem, true>(a.y, a.dx, a.c, xrows, tw, stream);
+  if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, St, true>(a.y, a.dx, a.c, xrows, tw, stream);
   // dX into dx, then its inverse in place; launches cover whole tokens
-  Elem* dx = static_cast<Elem*>(a.dx);
+  ElemOf<St>* dx = static_cast<ElemOf<St>*>(a.dx);
   e = per_row_slots(a.tokens, xblocks * a.kb, [&](int64_t t0, int64_t nt, unsigned blocks) {
-    hipLaunchKernelGGL(mp_dx_product_kernel<Elem>, dim3(blocks), dim3(256), 0, stream,
-                       static_cast<const Elem*>(a.y) + t0 * a.q * (int64_t)N, static_cast<const Elem*>(a.c),
+    hipLaunchKernelGGL(mp_dx_product_kernel<St>, dim3(blocks), dim3(256), 0, stream,
+                       static_cast<const ElemOf<St>*>(a.y) + t0 * a.q * (int64_t)N, static_cast<const ElemOf<St>*>(a.c),
                        dx + t0 * a.kb * (int64_t)N, nt, a.q, a.kb, N, xblocks);
   });
   if (e != hipSuccess) return e;
@@ -370,11 +346,12 @@ hipError_t mp_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, i
 }
 
 using MpFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t, int);
+using SeqMp = std::make_integer_sequence<int, kMpMaxLogN - kMpMinLogN + 1>;
+using MpRow = std::array<MpFn, kMpMaxLogN - kMpMinLogN + 1>;
 
-template <int... L>
-std::array<MpFn, sizeof...(L)> mp_table(bool bf16, bool backward, std::integer_sequence<int, L...>) {
-  return {(backward ? (bf16 ? &mp_backward<L + kMpMinLogN, uint32_t> : &mp_backward<L + kMpMinLogN, float2>)
-                    : (bf16 ? &mp_forward<L + kMpMinLogN, uint32_t> : &mp_forward<L + kMpMinLogN, float2>))...};
+template <class St, int... L>
+MpRow mp_row(bool backward, std::integer_sequence<int, L...>) {
+  return {(backward ? &mp_backward<L + kMpMinLogN, St> : &mp_forward<L + kMpMinLogN, St>)...};
 }
 
 }  // namespace
@@ -389,15 +366,21 @@ bool bca_multipass_supported(int logp, int q, int kb, bool backward) {
 
 hipError_t launch_bca_circulant(const BcaArgs& a, const float2* tw, hipStream_t stream) {
   if (a.logp - 1 != kCirculantLogN || a.q != 1 || a.kb != 1) return hipErrorInvalidValue;
-  return a.bf16 ? circulant_rows<kCirculantLogN, uint32_t>(a.x, a.y, a.c, a.tokens, tw, stream)
-                : circulant_rows<kCirculantLogN, float2>(a.x, a.y, a.c, a.tokens, tw, stream);
+  switch (a.storage) {
+    case kStorageF32: return circulant_rows<kCirculantLogN, StoreF32>(a.x, a.y, a.c, a.tokens, tw, stream);
+    case kStorageBF16: return circulant_rows<kCirculantLogN, StoreBF16>(a.x, a.y, a.c, a.tokens, tw, stream);
+    case kStorageF16: return circulant_rows<kCirculantLogN, StoreF16>(a.x, a.y, a.c, a.tokens, tw, stream);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_bca_multipass(const BcaArgs& a, bool backward, const float2* tw, hipStream_t stream, int num_cu) {
-  static const auto seq = std::make_integer_sequence<int, kMpMaxLogN - kMpMinLogN + 1>{};
-  static const std::array<MpFn, kMpMaxLogN - kMpMinLogN + 1> tab[2][2] = {
-      {mp_table(false, false, seq), mp_table(true, false, seq)}, {mp_table(false, true, seq), mp_table(true, true, seq)}};
-  return tab[backward ? 1 : 0][a.bf16 ? 1 : 0][a.logp - 1 - kMpMinLogN](a, tw, stream, num_cu);
+  // [direction][storage]
+  static const MpRow tab[2][3] = {
+      {mp_row<StoreF32>(false, SeqMp{}), mp_row<StoreBF16>(false, SeqMp{}), mp_row<StoreF16>(false, SeqMp{})},
+      {mp_row<StoreF32>(true, SeqMp{}), mp_row<StoreBF16>(true, SeqMp{}), mp_row<StoreF16>(true, SeqMp{})}};
+  if (a.storage < 0 || a.storage > 2) return hipErrorInvalidValue;
+  return tab[backward ? 1 : 0][a.storage][a.logp - 1 - kMpMinLogN](a, tw, stream, num_cu);
 }
 
 }  // namespace rdfft

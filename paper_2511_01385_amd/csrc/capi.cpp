@@ -125,8 +125,7 @@ struct BcaShape {
 
 int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t d_out, int64_t p, int64_t tokens,
               int dtype, bool backward, BcaShape* sh) {
-  if (dtype == RDFFT_F16) return RDFFT_EUNSUPPORTED;  // the layer kernels store f32 or bf16
-  if (dtype != RDFFT_F32 && dtype != RDFFT_BF16) return RDFFT_EINVAL;
+  if (dtype != RDFFT_F32 && dtype != RDFFT_BF16 && dtype != RDFFT_F16) return RDFFT_EINVAL;
   if (tokens < 0 || d_in <= 0 || d_out <= 0 || p <= 0) return RDFFT_EINVAL;
   if (p < 2 || (p & 1)) return RDFFT_EINVAL;
   if (d_in % p != 0 || d_out % p != 0) return RDFFT_EINVAL;
@@ -188,7 +187,7 @@ int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grad
   int num_cu = 0;
   st = ensure_device(&tw, &num_cu);
   if (st != RDFFT_OK) return st;
-  rdfft::BcaArgs a{x, c_spectra, y, nullptr, nullptr, tokens, sh.q, sh.kb, sh.logp, dtype == RDFFT_BF16};
+  rdfft::BcaArgs a{x, c_spectra, y, nullptr, nullptr, tokens, sh.q, sh.kb, sh.logp, dtype};
   return rdfft::launch_bca_forward(a, tw, reinterpret_cast<hipStream_t>(stream), num_cu) == hipSuccess
              ? RDFFT_OK
              : RDFFT_ELAUNCH;
@@ -223,7 +222,7 @@ int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* gr
   int num_cu = 0;
   st = ensure_device(&tw, &num_cu);
   if (st != RDFFT_OK) return st;
-  rdfft::BcaArgs a{x, c_spectra, gy, dx, dc, tokens, sh.q, sh.kb, sh.logp, dtype == RDFFT_BF16};
+  rdfft::BcaArgs a{x, c_spectra, gy, dx, dc, tokens, sh.q, sh.kb, sh.logp, dtype};
   return rdfft::launch_bca_backward(a, tw, reinterpret_cast<hipStream_t>(stream), num_cu) == hipSuccess
              ? RDFFT_OK
              : RDFFT_ELAUNCH;

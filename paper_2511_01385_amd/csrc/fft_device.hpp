@@ -173,6 +173,7 @@ struct GlobalF32 {
   using raw_t = float2;
   float2* base;
   __device__ __forceinline__ static float2 widen(raw_t r) { return r; }
+  __device__ __forceinline__ static raw_t narrow(float2 v) { return v; }
   __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return base[m]; }
   __device__ __forceinline__ void store(int m, float2 v) const { base[m] = v; }
@@ -193,6 +194,7 @@ struct GlobalBF16 {
   using raw_t = uint32_t;
   uint32_t* base;
   __device__ __forceinline__ static float2 widen(raw_t r) { return bf16x2_to_f32(r); }
+  __device__ __forceinline__ static raw_t narrow(float2 v) { return f32_to_bf16x2(v); }
   __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return bf16x2_to_f32(base[m]); }
   __device__ __forceinline__ void store(int m, float2 v) const { base[m] = f32_to_bf16x2(v); }
@@ -213,6 +215,7 @@ struct GlobalF16 {
   using raw_t = uint32_t;
   uint32_t* base;
   __device__ __forceinline__ static float2 widen(raw_t r) { return f16x2_to_f32(r); }
+  __device__ __forceinline__ static raw_t narrow(float2 v) { return f32_to_f16x2(v); }
   __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return f16x2_to_f32(base[m]); }
   __device__ __forceinline__ void store(int m, float2 v) const { base[m] = f32_to_f16x2(v); }
@@ -233,6 +236,39 @@ struct ConstBF16 {
   __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
   __device__ __forceinline__ float2 load(int m) const { return bf16x2_to_f32(base[m]); }
 };
+struct ConstF16 {
+  using raw_t = uint32_t;
+  const uint32_t* base;
+  __device__ __forceinline__ static float2 widen(raw_t r) { return f16x2_to_f32(r); }
+  __device__ __forceinline__ raw_t load_raw(int m) const { return base[m]; }
+  __device__ __forceinline__ float2 load(int m) const { return f16x2_to_f32(base[m]); }
+};
+
+// Storage types of the layer kernels: the pair type in memory (Elem), its read-only and
+// read-write row accessors, and the value of rdfft_dtype_t it stands for.  bf16 and f16
+// share the 32-bit pair type, so the layer kernels are instantiated per storage struct.
+struct StoreF32 {
+  using Elem = float2;
+  using In = ConstF32;
+  using Out = GlobalF32;
+  static constexpr int kId = 0;
+  static constexpr bool kHalf = false;
+};
+struct StoreBF16 {
+  using Elem = uint32_t;
+  using In = ConstBF16;
+  using Out = GlobalBF16;
+  static constexpr int kId = 1;
+  static constexpr bool kHalf = true;
+};
+struct StoreF16 {
+  using Elem = uint32_t;
+  using In = ConstF16;
+  using Out = GlobalF16;
+  static constexpr int kId = 2;
+  static constexpr bool kHalf = true;
+};
+
 
 // A packed spectrum kept in a row's (padded) LDS region
 struct LdsSpectrum {

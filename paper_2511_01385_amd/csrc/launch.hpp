@@ -46,7 +46,7 @@ struct BcaArgs {
   float* dc;          // backward only
   int64_t tokens;
   int q, kb, logp;    // p = 2^logp
-  bool bf16;
+  int storage;        // kStorageF32, kStorageBF16 or kStorageF16
 };
 
 hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu);

@@ -60,7 +60,7 @@ class _BcaFunction(torch.autograd.Function):
 class BlockCirculantLinear(torch.nn.Module):
     """y = W x with W (d_out x d_in) made of p x p circulant blocks (first columns c).
 
-    x has shape (..., d_in) and the storage type ``dtype`` (bfloat16 or float32); y has
+    x has shape (..., d_in) and the storage type ``dtype`` (bfloat16, float16 or float32); y has
     shape (..., d_out).  p must be a power of two with 2 <= p <= 65536 dividing d_in and
     d_out; blocks longer than 8192 also need d_in <= d_out and d_in <= 8p (their forward
     stages the input spectra in y).  c is initialised N(0, sigma^2) with sigma = d_in^-1/2
@@ -78,8 +78,8 @@ class BlockCirculantLinear(torch.nn.Module):
             raise ValueError(f"p = {p} is beyond the largest supported block, 65536")
         if p > 8192 and (d_in > d_out or d_in > 8 * p):
             raise ValueError(f"blocks of p = {p} > 8192 need d_in <= d_out and d_in <= 8p")
-        if dtype not in (torch.bfloat16, torch.float32):
-            raise TypeError(f"storage type must be bfloat16 or float32, got {dtype}")
+        if dtype not in (torch.bfloat16, torch.float16, torch.float32):
+            raise TypeError(f"storage type must be bfloat16, float16 or float32, got {dtype}")
         self.d_in, self.d_out, self.p = d_in, d_out, p
         self.dtype = dtype
         self.clobber_grad = clobber_grad

@@ -51,3 +51,21 @@ def test_short_run_prints_one_complete_json_line():
     # the reference rates beside the roofline: a device copy and an in-place pass over 1 GiB
     for ref in ("hbm_copy", "hbm_inplace"):
         assert d[ref]["GB_s"] > 0, ref
+
+
+def test_cpu_baseline_reports_all_cores_and_one():
+    """The oracle baseline on a tiny sample: an all-core figure with its worker count, and a
+    one-core figure beside it."""
+    sys.path.insert(0, ROOT)
+    import bench
+    from paper_2511_01385_amd import inputs
+
+    ns = [64, 128]
+    rows = {n: inputs.normal_rows(inputs.seed_for(2, salt=n), 32, n, "bf16") for n in ns}
+    lay = dict(tokens=8, d=256, p=64, sigma=0.02)
+    xcg = inputs.bca_problem(inputs.seed_for(4), 8, 256, 256, 64, 0.02, "bf16")
+    r = bench.cpu_baseline(rows, xcg, ns=ns, bca=lay, min_seconds=0.05, max_workers=2)
+    assert r["kind"] == "oracle" and r["unit"] == "GB/s" and r["value"] > 0
+    assert 1 <= r["cores"] <= 2 and r["cores"] <= len(os.sched_getaffinity(0))
+    assert r["single_core"]["cores"] == 1 and r["single_core"]["value"] > 0
+    assert "sample" in r and "sample" in r["single_core"]

@@ -116,7 +116,7 @@ def _grads(dx, dc):
         (A, B, A + (1 << 29), 256, 256, 64, -1, F32, EINVAL),
         (A, B, A + (1 << 29), 0, 256, 64, 8, F32, EINVAL),
         (A, B, A + (1 << 29), 256, 256, 64, 8, 5, EINVAL),
-        (A, B, A + (1 << 29), 256, 256, 64, 8, _lib.RDFFT_F16, EUNSUP),  # the layer stores f32 or bf16
+        (A, B, A + (1 << 29), 96, 96, 48, 8, _lib.RDFFT_F16, EUNSUP),  # f16 layer, p not a power of two
         (0, B, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # null x
         (A, 0, A + (1 << 29), 256, 256, 64, 8, F32, EINVAL),  # null spectra
         (A, B, 0, 256, 256, 64, 8, F32, EINVAL),  # null y

@@ -51,10 +51,13 @@ SMALL = [
     (5, 8192, 8192, 4096, "f32"),
     (4, 6144, 6144, 2048, "bf16"),
     (9, 256, 256, 16, "f32"),
-    # layers whose dC slots exceed LDS: one dx launch, then dC over block ranges
+    # layers whose dC slots exceed LDS: dC over block ranges, then one dx launch
     (5, 4096, 4096, 128, "bf16"),
     (3, 2048, 4096, 64, "f32"),
     (7, 4096, 2048, 256, "f32"),
+    # a token's spectra beyond the forward's two-workgroups-per-CU budget (8 x 8 blocks of 1024)
+    (3, 8192, 8192, 1024, "bf16"),
+    (2, 8192, 8192, 1024, "f32"),
 ]
 
 
@@ -84,9 +87,14 @@ def _run(x, c, g, dtype, d_out, alias_y=False, alias_dx=False):
 
 
 def _dc_bar(dtype, p):
-    # blocks beyond 8192 keep a bf16 layer's intermediate spectra in bf16, so its dc meets
-    # the bf16 bar; every other dc is float32 arithmetic on exactly widened inputs
-    return "bf16" if dtype == "bf16" and p > 8192 else "f32"
+    # blocks beyond 8192 keep a 16-bit layer's intermediate spectra in its storage type, so
+    # its dc meets that type's bar; every other dc is float32 arithmetic on exactly widened
+    # inputs
+    return dtype if dtype != "f32" and p > 8192 else "f32"
+
+
+# relative bound of sampled entries against the dense definition's sums, per storage type
+SAMPLE_RTOL = {"f32": 1e-4, "bf16": 2e-2, "f16": 2e-3}
 
 
 def _check(x, c, g, dtype, d_out, p, got, what, sampled=0):
@@ -107,15 +115,15 @@ def _check(x, c, g, dtype, d_out, p, got, what, sampled=0):
         # element bound's size, in units of the output's RMS
         spread = 4 * np.sqrt(staged) * ELEMENT_REL[dtype]
         ref = obca.forward_entries(x64, ceff, ent)
-        np.testing.assert_allclose([y[a, i * p + m] for a, i, m in ent], ref, rtol=2e-2 if dtype == "bf16" else 1e-4,
+        np.testing.assert_allclose([y[a, i * p + m] for a, i, m in ent], ref, rtol=SAMPLE_RTOL[dtype],
                                    atol=1e-3 * np.abs(ref).max() + spread * np.sqrt(np.mean(y**2)))
         ent = [(int(a), int(rng.integers(kb)), int(rng.integers(p))) for a in t_]
         ref = obca.dx_entries(g64, ceff, ent)
-        np.testing.assert_allclose([dx[a, j * p + r] for a, j, r in ent], ref, rtol=2e-2 if dtype == "bf16" else 1e-4,
+        np.testing.assert_allclose([dx[a, j * p + r] for a, j, r in ent], ref, rtol=SAMPLE_RTOL[dtype],
                                    atol=1e-3 * np.abs(ref).max() + spread * np.sqrt(np.mean(dx**2)))
         ent = [(int(rng.integers(q)), int(rng.integers(kb)), int(rng.integers(p))) for _ in range(4)]
         ref = obca.dc_entries(x64, g64, q, kb, p, ent)
-        tol = 1e-4 if _dc_bar(dtype, p) == "f32" else 2e-2
+        tol = SAMPLE_RTOL[_dc_bar(dtype, p)]
         np.testing.assert_allclose([dc[i, j, s] for i, j, s in ent], ref, rtol=tol,
                                    atol=tol * np.abs(ref).max() + spread * np.sqrt(np.mean(dc**2)))
 
@@ -194,6 +202,42 @@ def test_square_layer_dc_sums(shape):
     x, c, g = _problem(606 + tokens, tokens, d, d, p, 0.01, dtype)
     got = _run(x, c, g, dtype, d, alias_dx=alias)
     _check(x, c, g, dtype, d, p, got, str(shape))
+
+
+# float16 storage: the 256-, 768- and 4096-wide paper-shaped layers at full size, the
+# 8192-wide circulant, and shapes that reach every other kernel family (general kernels,
+# split dC, blocks beyond 8192, the fused single-circulant row kernel)
+F16 = [
+    (128, 256, 256, 64, 0.02, 17),
+    (4096, 768, 768, 256, 0.02, 17),
+    (4096, 4096, 4096, 1024, 0.01, 17),
+    (96, 8192, 8192, 8192, 0.02, 0),
+    (37, 512, 256, 128, 0.05, 0),
+    (5, 4096, 4096, 128, 0.05, 0),
+    (3, 16384, 16384, 16384, 0.004, 3),
+    (6, 32768, 32768, 32768, 0.004, 0),
+]
+
+
+@pytest.mark.parametrize("shape", F16, ids=[f"T{s[0]}_{s[1]}x{s[2]}_p{s[3]}" for s in F16])
+def test_f16_layers(shape):
+    tokens, d_in, d_out, p, sigma, sampled = shape
+    x, c, g = _problem(9090 + tokens, tokens, d_in, d_out, p, sigma, "f16")
+    got = _run(x, c, g, "f16", d_out)
+    _check(x, c, g, "f16", d_out, p, got, f"f16 {shape}", sampled=sampled)
+
+
+# square layers whose dC slots exceed LDS, with dx == gy: the dC launches read gy, so they
+# must all run before the dx launch overwrites it
+SPLIT_ALIASED = [(5, 4096, 128, "bf16"), (3, 4096, 512, "f32"), (4, 4096, 512, "bf16"), (3, 8192, 1024, "bf16")]
+
+
+@pytest.mark.parametrize("shape", SPLIT_ALIASED, ids=[f"T{s[0]}_{s[1]}_p{s[2]}_{s[3]}" for s in SPLIT_ALIASED])
+def test_split_dc_with_dx_over_gy(shape):
+    tokens, d, p, dtype = shape
+    x, c, g = _problem(808 + tokens, tokens, d, d, p, 0.02, dtype)
+    got = _run(x, c, g, dtype, d, alias_dx=True)
+    _check(x, c, g, dtype, d, p, got, f"{shape} dx over gy")
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])

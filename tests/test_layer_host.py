@@ -15,7 +15,8 @@ def test_rejects_bad_block_sizes(d_in, d_out, p):
 
 def test_rejects_unsupported_storage_type():
     with pytest.raises(TypeError):
-        BlockCirculantLinear(64, 64, 16, dtype=torch.float16, device="cpu")
+        BlockCirculantLinear(64, 64, 16, dtype=torch.float64, device="cpu")
+    BlockCirculantLinear(64, 64, 16, dtype=torch.float16, device="cpu")  # 16-bit IEEE storage is supported
 
 
 def test_parameter_shape_and_scale():
