@@ -2,30 +2,84 @@
 // to the kernels of bca_kernels.hpp (instantiated per storage type in
 // bca_store_{f32,bf16,f16}.hip) and the multi-pass layer of bca_multipass.hip, plus the
 // two small kernels every storage type shares: the fill of dc and the second stage of
-// the two-stage dC sum.
+// the two-stage dC sum (fused with dc's inverse transform).
 #include <hip/hip_runtime.h>
 
 #include "bca_kernels.hpp"
 
 namespace rdfft {
 
-// Second stage of the two-stage dC sum: dc[e] += the partials of workgroups
-// b in [blockIdx.y*kReduceGroup, +kReduceGroup) (zeroed dc, one float32 atomic pair per
-// thread and group of workgroups).  Workgroup b's slot e lies at
-// stage[(b + c*groups)*tile_f2 + e - c*chunk], c = e / chunk.
-__global__ void __launch_bounds__(256) bca_dc_reduce_kernel(const float2* __restrict__ stage, float* __restrict__ dc,
-                                                            int qkn, int chunk, int groups, int64_t tile_f2) {
-  const int e = blockIdx.x * 256 + threadIdx.x;
-  if (e >= qkn) return;
-  const int ch = e / chunk;
-  const int b0 = blockIdx.y * kReduceGroup;
+// Second stage of the two-stage dC sum, fused with the inverse transform of dc.  A
+// workgroup takes one (i, j) row of dC and one group of kReduceGroup workgroups' partial
+// sums: its threads add those partials slot by slot into an LDS region, the row's
+// threads transform the sum to the time domain in place and add the result into dc
+// (zeroed beforehand) with float32 atomics.  The inverse transform is linear, so the sum over the groups of the
+// transformed group sums is the transform of the full sum.  Workgroup b's partial of
+// slot e = ij*N + k lies at stage[(b + c*groups)*tile_f2 + e - c*chunk], c = e / chunk.
+struct AtomicAddF32 {  // a time-domain row of dc, added into
+  float* base;
+  __device__ __forceinline__ void store(int m, float2 v) const {
+    unsafeAtomicAdd(base + 2 * m, v.x);
+    unsafeAtomicAdd(base + 2 * m + 1, v.y);
+  }
+};
+
+// threads of the finish kernel: a row of more than 64 threads synchronises with workgroup
+// barriers, so the workgroup is that one row; shorter rows synchronise at wave level only,
+// and the workgroup keeps the row kernels' size, its other threads helping with the sums
+template <int LOGN>
+constexpr int finish_wg() {
+  return RowPlan<LOGN>::TPR > 64 ? RowPlan<LOGN>::TPR : RowPlan<LOGN>::WG;
+}
+
+template <int LOGN>
+__global__ void __launch_bounds__(finish_wg<LOGN>()) bca_dc_finish_kernel(const float2* __restrict__ stage,
+                                                                          float* __restrict__ dc, int rows_ij,
+                                                                          int chunk, int groups, int64_t tile_f2,
+                                                                          const float2* __restrict__ tw) {
+  using P = RowPlan<LOGN>;
+  constexpr int N = P::N, TPR = P::TPR, WG = finish_wg<LOGN>();
+  constexpr int REG = P::LDS_F2 > lds_padded_size(N) ? P::LDS_F2 : lds_padded_size(N);
+  __shared__ float2 reg[REG];
+  // one unit per workgroup: every thread sums slots, then the first row group transforms
+  const int ij = blockIdx.x % rows_ij, gg = blockIdx.x / rows_ij;
+  const int b0 = gg * kReduceGroup;
   const int b1 = b0 + kReduceGroup < groups ? b0 + kReduceGroup : groups;
-  const float2* p = stage + ((int64_t)ch * groups + b0) * tile_f2 + (e - ch * chunk);
-  float2 v = make_float2(0.f, 0.f);
+  for (int k = threadIdx.x; k < N; k += WG) {
+    const int e = ij * N + k;
+    const int ch = e / chunk;
+    const float2* p = stage + ((int64_t)ch * groups + b0) * tile_f2 + (e - ch * chunk);
+    float2 v = make_float2(0.f, 0.f);
 #pragma unroll 8
-  for (int b = b0; b < b1; ++b, p += tile_f2) v = c_add(v, *p);
-  unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
-  unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
+    for (int b = b0; b < b1; ++b, p += tile_f2) v = c_add(v, *p);
+    reg[lds_pad(k)] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < TPR)  // the whole workgroup when TPR > 64
+    row_inverse<LOGN, true>((int)threadIdx.x, true, LdsSpectrum{reg}, AtomicAddF32{dc + (int64_t)ij * 2 * N}, reg, tw);
+}
+
+template <int LOGN>
+static hipError_t dc_finish_launch(const float2* stage, float* dc, int rows_ij, int chunk, int groups, int64_t tile_f2,
+                                   const float2* tw, hipStream_t stream) {
+  const int units = rows_ij * ((groups + kReduceGroup - 1) / kReduceGroup);
+  hipLaunchKernelGGL(bca_dc_finish_kernel<LOGN>, dim3((unsigned)units), dim3(finish_wg<LOGN>()), 0, stream, stage, dc,
+                     rows_ij, chunk, groups, tile_f2, tw);
+  return hipGetLastError();
+}
+
+template <int... L>
+static std::array<hipError_t (*)(const float2*, float*, int, int, int, int64_t, const float2*, hipStream_t),
+                  sizeof...(L)>
+dc_finish_table(std::integer_sequence<int, L...>) {
+  return {&dc_finish_launch<L>...};
+}
+
+hipError_t launch_dc_finish(const float2* stage, float* dc, int rows_ij, int logn, int chunk, int groups,
+                            int64_t tile_f2, const float2* tw, hipStream_t stream) {
+  static const auto tab = dc_finish_table(std::make_integer_sequence<int, kBcaMaxLogN + 1>{});
+  if (logn < 0 || logn > kBcaMaxLogN) return hipErrorInvalidValue;
+  return tab[logn](stage, dc, rows_ij, chunk, groups, tile_f2, tw, stream);
 }
 
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
@@ -36,13 +90,6 @@ __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
 hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t stream) {
   const int blocks = (int)std::min<int64_t>((count + 255) / 256, 1024);
   hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, stream, p, count);
-  return hipGetLastError();
-}
-
-hipError_t launch_dc_reduce(const float2* stage, float* dc, int qkn, int chunk, int groups, int64_t tile_f2,
-                            hipStream_t stream) {
-  const dim3 rgrid((unsigned)((qkn + 255) / 256), (unsigned)((groups + kReduceGroup - 1) / kReduceGroup));
-  hipLaunchKernelGGL(bca_dc_reduce_kernel, rgrid, dim3(256), 0, stream, stage, dc, qkn, chunk, groups, tile_f2);
   return hipGetLastError();
 }
 
@@ -70,7 +117,8 @@ hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t st
   if (a.logp - 1 > kBcaMaxLogN) return launch_bca_multipass(a, false, tw, stream, num_cu);
   if (a.logp - 1 == kCirculantLogN && a.q == 1 && a.kb == 1) return launch_bca_circulant(a, tw, stream);
   if (a.q == a.kb && a.q <= kSqMaxBlocks) {
-    const BcaBwdFn fn = t.sq_fwd[a.q - 1][a.logp - 1];
+    BcaBwdFn fn = t.wave_fwd[a.q - 1][a.logp - 1];
+    if (fn == nullptr) fn = t.sq_fwd[a.q - 1][a.logp - 1];
     if (fn != nullptr) return fn(a, tw, stream, num_cu);
   }
   return t.fwd[a.logp - 1](a, tw, stream);
@@ -83,16 +131,18 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
   // the square-layer kernels zero dc themselves (in the kernel when the dC sum is staged);
   // every other path finds it zeroed
   BcaBwdFn sq_fn = nullptr;
-  if (a.tokens > 0 && a.logp - 1 <= kBcaMaxLogN && a.q == a.kb && a.q <= kSqMaxBlocks)
-    sq_fn = t.sq_bwd[a.q - 1][a.logp - 1];
+  if (a.tokens > 0 && a.logp - 1 <= kBcaMaxLogN && a.q == a.kb && a.q <= kSqMaxBlocks) {
+    sq_fn = t.wave_bwd[a.q - 1][a.logp - 1];
+    if (sq_fn == nullptr) sq_fn = t.sq_bwd[a.q - 1][a.logp - 1];
+  }
   hipError_t e = hipSuccess;
   if (sq_fn == nullptr) {
     e = launch_fill_zero(a.dc, slots, stream);
     if (e != hipSuccess || a.tokens == 0) return e;
   }
-  if (sq_fn != nullptr) {
-    e = sq_fn(a, tw, stream, num_cu);
-  } else if (a.logp - 1 > kBcaMaxLogN) {
+  // the square-layer kernels also leave dc in the time domain
+  if (sq_fn != nullptr) return sq_fn(a, tw, stream, num_cu);
+  if (a.logp - 1 > kBcaMaxLogN) {
     e = launch_bca_multipass(a, true, tw, stream, num_cu);
   } else {
     e = t.bwd[a.logp - 1](a, tw, stream, num_cu);

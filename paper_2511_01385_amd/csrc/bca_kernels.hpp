@@ -519,7 +519,7 @@ __global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const ElemOf<St>* _
   if (stage != nullptr) {
     // Two-stage sum (dx is not gy): the partial sums go to the gy rows of this workgroup's
     // first tiles, which it alone has read and nobody reads again, chunk c of them (chunk
-    // float2 each) to tile blockIdx.x + c*gridDim.x; bca_dc_reduce_kernel then adds the
+    // float2 each) to tile blockIdx.x + c*gridDim.x; bca_dc_finish_kernel then adds the
     // workgroups' partials into dc.
     for (int e = tid; e < QKN; e += WG) {
       float2 v = part[e];
@@ -540,11 +540,14 @@ __global__ void __launch_bounds__(WG) bca_backward_sq_kernel(const ElemOf<St>* _
   }
 }
 
-// Second stage of the two-stage dC sum and the fill of dc (bca_kernels.hip)
+// The fill of dc, and the second stage of the two-stage dC sum (bca_kernels.hip): the
+// staged partials of `groups` workgroups for rows_ij rows of n = 2^(logn+1), summed in
+// groups of kReduceGroup workgroups, transformed to the time domain and added into the
+// zeroed dc.
 constexpr int kReduceGroup = 16;
 constexpr int64_t kStageMinAtomics = (int64_t)1 << 21;
-hipError_t launch_dc_reduce(const float2* stage, float* dc, int qkn, int chunk, int groups, int64_t tile_f2,
-                            hipStream_t stream);
+hipError_t launch_dc_finish(const float2* stage, float* dc, int rows_ij, int logn, int chunk, int groups,
+                            int64_t tile_f2, const float2* tw, hipStream_t stream);
 hipError_t launch_fill_zero(float* p, int64_t count, hipStream_t stream);
 
 // ----------------------------------------------------------------------------------
@@ -777,8 +780,327 @@ static hipError_t bwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t st
                      static_cast<const ElemOf<St>*>(a.x), static_cast<const ElemOf<St>*>(a.c), static_cast<const ElemOf<St>*>(a.y),
                      static_cast<ElemOf<St>*>(a.dx), a.dc, a.tokens, TT, tiles, stage, tile_f2, chunk, tw);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || !staged) return e;
-  return launch_dc_reduce(stage, a.dc, QKN, chunk, (int)grid, tile_f2, stream);
+  if (e != hipSuccess) return e;
+  if (staged) return launch_dc_finish(stage, a.dc, QB * QB, LOGN, chunk, (int)grid, tile_f2, tw, stream);
+  // dc holds sum_t conj(X) . G as packed spectra; transform them in place to the time domain
+  return launch_rdfft_rows(a.dc, (int64_t)QB * QB, LOGN, kStorageF32, true, tw, stream, num_cu);
+}
+
+// ----------------------------------------------------------------------------------
+// Square layers (q == kb == QB) with short blocks, whose rows fit inside one wavefront
+// (TPR <= 64, at least 64 bins).  Every wave works on its own groups of TW tokens: its
+// transforms, per-bin products and inverse transforms synchronise at wave level only, so
+// no wave waits for another; a workgroup's waves share nothing but the backward's final
+// dC reduction.  Lane l owns bins l, l + 64, ... (BL of them): it reads C_ij[k] for a bin
+// once per group (from L1/L2: C is small) and, in the backward, keeps its dC_ij[k] sums in
+// registers for the whole kernel.
+//
+// Each group first takes a copy of the twiddle pointer that the compiler cannot see
+// through: otherwise it hoists the loop-invariant twiddle reads of every transform out of
+// the group loop and keeps them all in registers, which spilled.
+template <int LOGN, int QB>
+struct BcaWave {
+  using P = RowPlan<LOGN>;
+  static constexpr int N = P::N, TPR = P::TPR;
+  static constexpr int G = TPR <= 64 ? 64 / TPR : 1;  // rows one wave transforms at a time
+  static constexpr int BL = N >= 64 ? N / 64 : 1;      // bins per lane
+  static constexpr int REG = BcaPlan<LOGN>::REGION;
+  static constexpr int CS = BL * QB * QB;                // dC slots per lane
+};
+// waves per workgroup: the forward's workgroups are independent sets of waves; the
+// backward runs one wider workgroup per CU, whose waves add their dC before it leaves
+constexpr int kWaveFwdNW = 4, kWaveBwdNW = 8;
+// asked of the compiler: at least this many waves per SIMD (at most 128 VGPRs), so that a
+// CU keeps enough waves in flight to cover their memory and LDS latency.  The backward
+// runs one workgroup of kWaveBwdNW waves per CU, two per SIMD, so more registers cost it
+// nothing (and its dC sums live in them).
+constexpr int kWaveMinWaves = 4, kWaveBwdMinWaves = 2;
+
+template <int LOGN, int QB>
+constexpr bool wave_fits(bool backward) {
+  using W = BcaWave<LOGN, QB>;
+  return W::TPR <= 64 && W::N >= 64 && W::N <= 256 && (backward ? W::CS <= 18 : W::CS <= 32);
+}
+
+// Tokens per wave group: the rows of a group (QB per token and direction) fill whole
+// rounds of G row slots where that keeps a wave's LDS small; otherwise short groups.
+template <int LOGN, int QB>
+constexpr int wave_tokens() {
+  constexpr int G = BcaWave<LOGN, QB>::G;
+  return G % QB == 0 ? G / QB : (G >= 2 * QB ? G / QB : 1);
+}
+
+// Forward: per group, X_j = rdFFT(x_j) into the wave's LDS regions, Y_i = sum_j C_ij X_j
+// per bin written over X_i (a lane reads every X_j[k] of its bin before it writes), then
+// y_i = irdFFT(Y_i).  y may be x: a wave reads its group's x rows before it writes the
+// group's y rows, and no other wave touches them.
+template <int LOGN, class St, int QB, int TW, int NW = kWaveFwdNW>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWaveMinWaves)))
+bca_forward_wave_kernel(const ElemOf<St>* x, const ElemOf<St>* __restrict__ c,
+                                                                   ElemOf<St>* y, int64_t tokens, int64_t ngroups,
+                                                                   const float2* __restrict__ tw) {
+  using W = BcaWave<LOGN, QB>;
+  using In = typename St::In;
+  using Out = typename St::Out;
+  constexpr int N = W::N, TPR = W::TPR, G = W::G, BL = W::BL, REG = W::REG;
+  constexpr int NR = TW * QB, ROUNDS = (NR + G - 1) / G;
+  constexpr int WREGS = NR + (NR % G != 0 ? 1 : 0);  // + a spare region for idle row slots
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / TPR, t = lane - grp * TPR;
+  float2* const xs = bca_lds + (size_t)wave * WREGS * REG;
+  float2* const spare = xs + (size_t)NR * REG;
+  const int64_t wstride = (int64_t)gridDim.x * NW;
+  for (int64_t gi = (int64_t)blockIdx.x * NW + wave; gi < ngroups; gi += wstride) {
+    const int64_t tok0 = gi * TW;
+    const int nvalid = (int)(tokens - tok0 < TW ? tokens - tok0 : TW);
+    const float2* twg = tw;
+    asm volatile("" : "+s"(twg));
+    // (runtime loops over the rounds: unrolled, the compiler hoists every round's loads)
+#pragma unroll 1
+    for (int r = 0; r < ROUNDS; ++r) {
+      const int s = r * G + grp;
+      const bool valid = s < NR;
+      const int tt = valid ? s / QB : 0, j = valid ? s - tt * QB : 0;
+      const bool act = valid && tt < nvalid;
+      float2* reg = valid ? xs + (size_t)s * REG : spare;
+      const In src{x + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N};
+      row_forward<LOGN, true>(t, act, src, LdsSpectrum{reg}, reg, twg);
+    }
+    row_sync<64>();
+    static_for<BL>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int k = lane + 64 * b;
+      typename In::raw_t cb[QB * QB];
+      {
+        const In cin{c};
+        static_for<QB * QB>([&](auto sc) { cb[decltype(sc)::value] = cin.load_raw(decltype(sc)::value * N + k); });
+      }
+      for (int tt = 0; tt < nvalid; ++tt) {
+        float2* xk = xs + (size_t)tt * QB * REG + lds_pad(k);
+        auto block_sum = [&](auto s0c) {
+          constexpr bool S0 = decltype(s0c)::value;
+          float2 X[QB];
+          static_for<QB>([&](auto jc) { X[decltype(jc)::value] = xk[decltype(jc)::value * REG]; });
+          static_for<QB>([&](auto ic) {
+            constexpr int i = decltype(ic)::value;
+            float2 a = make_float2(0.f, 0.f);
+            static_for<QB>([&](auto jc) {
+              constexpr int j = decltype(jc)::value;
+              a = slot_mac<S0, false>(a, In::widen(cb[i * QB + j]), X[j]);
+            });
+            xk[i * REG] = a;
+          });
+        };
+        if (b == 0 && lane == 0) block_sum(std::true_type{});
+        else block_sum(std::false_type{});
+      }
+    });
+    row_sync<64>();
+#pragma unroll 1
+    for (int r = 0; r < ROUNDS; ++r) {
+      const int s = r * G + grp;
+      const bool valid = s < NR;
+      const int tt = valid ? s / QB : 0, i = valid ? s - tt * QB : 0;
+      const bool act = valid && tt < nvalid;
+      float2* reg = valid ? xs + (size_t)s * REG : spare;
+      const Out dst{y + ((act ? tok0 + tt : 0) * QB + i) * (int64_t)N};
+      row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, twg);
+    }
+    row_sync<64>();  // the next group's transforms reuse the regions
+  }
+}
+
+// Backward: per group, X_j = rdFFT(x_j) and G_i = rdFFT(g_i) into LDS; per bin
+// dC_ij += conj(X_j) G_i (registers, summed over all of the wave's groups) and
+// dX_j = sum_i conj(C_ij) G_i written over X_j; dx_j = irdFFT(dX_j).  At the end the
+// workgroup's four waves add their dC in LDS, and the sum goes to dc by float32 atomics
+// (stage == nullptr; dc zeroed beforehand) or is written to `stage` at
+// blockIdx.x * stage_f2 for bca_dc_finish_kernel (then this kernel zeroes dc).
+template <int LOGN, class St, int QB, int TW, int NW = kWaveBwdNW>
+__global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWaveBwdMinWaves)))
+bca_backward_wave_kernel(const ElemOf<St>* __restrict__ x,
+                                                                    const ElemOf<St>* __restrict__ c,
+                                                                    const ElemOf<St>* gy, ElemOf<St>* dx,
+                                                                    float* __restrict__ dc, int64_t tokens,
+                                                                    int64_t ngroups, float2* stage, int64_t stage_f2,
+                                                                    const float2* __restrict__ tw) {
+  using W = BcaWave<LOGN, QB>;
+  using In = typename St::In;
+  using Out = typename St::Out;
+  constexpr int N = W::N, TPR = W::TPR, G = W::G, BL = W::BL, REG = W::REG, CS = W::CS;
+  constexpr int NR = TW * QB, NA = 2 * NR;
+  constexpr int ROUNDS_A = (NA + G - 1) / G, ROUNDS_C = (NR + G - 1) / G;
+  constexpr int WREGS = NA + (NA % G != 0 || NR % G != 0 ? 1 : 0);
+  constexpr int QKN = QB * QB * N;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int grp = lane / TPR, t = lane - grp * TPR;
+  float2* const xs = bca_lds + (size_t)wave * WREGS * REG;  // NR regions: X, then dX
+  float2* const gs = xs + (size_t)NR * REG;                   // NR regions: G
+  float2* const spare = xs + (size_t)NA * REG;
+  if (stage != nullptr) {
+    // the reduce kernel that adds into dc runs after this one on the stream
+    for (int64_t e = (int64_t)blockIdx.x * (64 * NW) + threadIdx.x; e < 2 * (int64_t)QKN;
+         e += (int64_t)gridDim.x * (64 * NW))
+      dc[e] = 0.f;
+  }
+  float2 dcr[CS];
+  static_for<CS>([&](auto sc) { dcr[decltype(sc)::value] = make_float2(0.f, 0.f); });
+
+  const int64_t wstride = (int64_t)gridDim.x * NW;
+  for (int64_t gi = (int64_t)blockIdx.x * NW + wave; gi < ngroups; gi += wstride) {
+    const int64_t tok0 = gi * TW;
+    const int nvalid = (int)(tokens - tok0 < TW ? tokens - tok0 : TW);
+    const float2* twg = tw;
+    asm volatile("" : "+s"(twg));
+#pragma unroll 1
+    for (int r = 0; r < ROUNDS_A; ++r) {
+      const int s = r * G + grp;
+      const bool valid = s < NA;
+      const int sx = s < NR ? s : s - NR;
+      const int tt = valid ? sx / QB : 0, j = valid ? sx - tt * QB : 0;
+      const bool act = valid && tt < nvalid;
+      float2* reg = valid ? xs + (size_t)s * REG : spare;
+      const ElemOf<St>* base = s < NR ? x : gy;
+      const In src{base + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N};
+      row_forward<LOGN, true>(t, act, src, LdsSpectrum{reg}, reg, twg);
+    }
+    row_sync<64>();
+    static_for<BL>([&](auto bc) {
+      constexpr int b = decltype(bc)::value;
+      const int k = lane + 64 * b;
+      typename In::raw_t cb[QB * QB];
+      {
+        const In cin{c};
+        static_for<QB * QB>([&](auto sc) { cb[decltype(sc)::value] = cin.load_raw(decltype(sc)::value * N + k); });
+      }
+      for (int tt = 0; tt < nvalid; ++tt) {
+        float2* xk = xs + (size_t)tt * QB * REG + lds_pad(k);
+        const float2* gk = gs + (size_t)tt * QB * REG + lds_pad(k);
+        auto contract = [&](auto s0c) {
+          constexpr bool S0 = decltype(s0c)::value;
+          float2 X[QB], Gv[QB];
+          static_for<QB>([&](auto jc) { X[decltype(jc)::value] = xk[decltype(jc)::value * REG]; });
+          static_for<QB>([&](auto ic) { Gv[decltype(ic)::value] = gk[decltype(ic)::value * REG]; });
+          static_for<QB>([&](auto jc) {
+            constexpr int j = decltype(jc)::value;
+            float2 d = make_float2(0.f, 0.f);
+            static_for<QB>([&](auto ic) {
+              constexpr int i = decltype(ic)::value, sl = b * QB * QB + i * QB + j;
+              dcr[sl] = slot_mac<S0, true>(dcr[sl], X[j], Gv[i]);
+              d = slot_mac<S0, true>(d, In::widen(cb[i * QB + j]), Gv[i]);
+            });
+            xk[j * REG] = d;
+          });
+        };
+        if (b == 0 && lane == 0) contract(std::true_type{});
+        else contract(std::false_type{});
+      }
+    });
+    row_sync<64>();
+#pragma unroll 1
+    for (int r = 0; r < ROUNDS_C; ++r) {
+      const int s = r * G + grp;
+      const bool valid = s < NR;
+      const int tt = valid ? s / QB : 0, j = valid ? s - tt * QB : 0;
+      const bool act = valid && tt < nvalid;
+      float2* reg = valid ? xs + (size_t)s * REG : spare;
+      const Out dst{dx + ((act ? tok0 + tt : 0) * QB + j) * (int64_t)N};
+      row_inverse<LOGN, true>(t, act, LdsSpectrum{reg}, dst, reg, twg);
+    }
+    row_sync<64>();
+  }
+
+  // the workgroup's dC: wave w's slot (i*QB + j)*N + k at part[w*QKN + ...]
+  __syncthreads();
+  float2* const part = bca_lds;
+  static_for<BL>([&](auto bc) {
+    constexpr int b = decltype(bc)::value;
+    static_for<QB * QB>([&](auto sc) {
+      constexpr int sl = decltype(sc)::value;
+      part[(size_t)wave * QKN + sl * N + lane + 64 * b] = dcr[b * QB * QB + sl];
+    });
+  });
+  __syncthreads();
+  if (stage != nullptr) {
+    for (int e = threadIdx.x; e < QKN; e += (64 * NW)) {
+      float2 v = part[e];
+      static_for<NW - 1>([&](auto wc) { v = c_add(v, part[(size_t)(decltype(wc)::value + 1) * QKN + e]); });
+      stage[(int64_t)blockIdx.x * stage_f2 + e] = v;
+    }
+    return;
+  }
+  const int shift = (int)(((unsigned)blockIdx.x * 64u) % (unsigned)QKN);
+  for (int e0 = threadIdx.x; e0 < QKN; e0 += (64 * NW)) {
+    int e = e0 + shift;
+    if (e >= QKN) e -= QKN;
+    float2 v = part[e];
+    static_for<NW - 1>([&](auto wc) { v = c_add(v, part[(size_t)(decltype(wc)::value + 1) * QKN + e]); });
+    unsafeAtomicAdd(dc + 2 * (int64_t)e, v.x);
+    unsafeAtomicAdd(dc + 2 * (int64_t)e + 1, v.y);
+  }
+}
+
+// LDS of one workgroup of the wave kernels
+template <int LOGN, int QB>
+constexpr size_t wave_lds_bytes(bool backward) {
+  using W = BcaWave<LOGN, QB>;
+  constexpr int TW = wave_tokens<LOGN, QB>(), NR = TW * QB;
+  const int nw = backward ? kWaveBwdNW : kWaveFwdNW;
+  const int na = backward ? 2 * NR : NR;
+  const bool spare = na % W::G != 0 || NR % W::G != 0;
+  const size_t spectra = (size_t)nw * (na + (spare ? 1 : 0)) * W::REG * sizeof(float2);
+  const size_t part = backward ? (size_t)nw * QB * QB * W::N * sizeof(float2) : 0;
+  return spectra > part ? spectra : part;
+}
+
+template <int LOGN, class St, int QB>
+static hipError_t fwd_wave_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  constexpr int TW = wave_tokens<LOGN, QB>(), NW = kWaveFwdNW;
+  constexpr size_t lds = wave_lds_bytes<LOGN, QB>(false);
+  static_assert(lds <= (size_t)kLdsLimit, "wave groups too large for LDS");
+  static const hipError_t attr = set_lds_limit(bca_forward_wave_kernel<LOGN, St, QB, TW>);
+  if (attr != hipSuccess) return attr;
+  const int64_t groups = (a.tokens + TW - 1) / TW;
+  // every wave takes groups until none are left; enough workgroups for a full chip
+  const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / (64 * NW)));
+  const int64_t grid = std::min<int64_t>((groups + NW - 1) / NW, (int64_t)num_cu * per_cu);
+  hipLaunchKernelGGL((bca_forward_wave_kernel<LOGN, St, QB, TW>), dim3((unsigned)grid), dim3(64 * NW), lds, stream,
+                     static_cast<const ElemOf<St>*>(a.x), static_cast<const ElemOf<St>*>(a.c),
+                     static_cast<ElemOf<St>*>(a.y), a.tokens, groups, tw);
+  return hipGetLastError();
+}
+
+template <int LOGN, class St, int QB>
+static hipError_t bwd_wave_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  using W = BcaWave<LOGN, QB>;
+  constexpr int TW = wave_tokens<LOGN, QB>(), NW = kWaveBwdNW;
+  constexpr size_t lds = wave_lds_bytes<LOGN, QB>(true);
+  static_assert(lds <= (size_t)kLdsLimit, "wave groups too large for LDS");
+  constexpr int QKN = QB * QB * W::N;
+  static const hipError_t attr = set_lds_limit(bca_backward_wave_kernel<LOGN, St, QB, TW>);
+  if (attr != hipSuccess) return attr;
+  const int64_t groups = (a.tokens + TW - 1) / TW;
+  // one workgroup per CU: fewer workgroups, fewer dC partial sums to add
+  const int64_t grid = std::min<int64_t>((groups + NW - 1) / NW, (int64_t)num_cu);
+  // Two-stage dC sum when dx has its own buffer: workgroup b's first groups are the
+  // tokens [b*NW*TW, (b+1)*NW*TW), whose gy rows only it reads; once all its waves are
+  // done it writes its partial sums there (QKN float2 must fit those rows, all of them
+  // valid tokens)
+  const int64_t region_f2 = (int64_t)NW * TW * QB * W::N * (int64_t)sizeof(ElemOf<St>) / (int64_t)sizeof(float2);
+  const bool staged = a.dx != a.y && region_f2 >= QKN && grid * NW * TW <= a.tokens;
+  float2* const stage = staged ? static_cast<float2*>(a.y) : nullptr;
+  if (!staged) {
+    const hipError_t ez = launch_fill_zero(a.dc, 2 * (int64_t)QKN, stream);
+    if (ez != hipSuccess) return ez;
+  }
+  hipLaunchKernelGGL((bca_backward_wave_kernel<LOGN, St, QB, TW>), dim3((unsigned)grid), dim3(64 * NW), lds, stream,
+                     static_cast<const ElemOf<St>*>(a.x), static_cast<const ElemOf<St>*>(a.c),
+                     static_cast<const ElemOf<St>*>(a.y), static_cast<ElemOf<St>*>(a.dx), a.dc, a.tokens, groups, stage,
+                     region_f2, tw);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  if (staged) return launch_dc_finish(stage, a.dc, QB * QB, LOGN, QKN, (int)grid, region_f2, tw, stream);
+  return launch_rdfft_rows(a.dc, (int64_t)QB * QB, LOGN, kStorageF32, true, tw, stream, num_cu);
 }
 
 using BcaFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t);
@@ -833,11 +1155,34 @@ struct BcaStoreTables {
   std::array<BcaBwdFn, kBcaMaxLogN + 1> bwd;
   SqTable sq_fwd;
   SqTable sq_bwd;
+  SqTable wave_fwd;
+  SqTable wave_bwd;
 };
+
+template <int LOGN, class St, int QB>
+static constexpr BcaBwdFn wave_entry(bool backward) {
+  if constexpr (wave_fits<LOGN, QB>(true)) {
+    return backward ? &bwd_wave_impl<LOGN, St, QB> : &fwd_wave_impl<LOGN, St, QB>;
+  } else if constexpr (wave_fits<LOGN, QB>(false)) {
+    return backward ? nullptr : &fwd_wave_impl<LOGN, St, QB>;
+  } else {
+    return nullptr;
+  }
+}
+template <class St, int QB, int... L>
+static std::array<BcaBwdFn, sizeof...(L)> wave_row(bool backward, std::integer_sequence<int, L...>) {
+  return {wave_entry<L, St, QB>(backward)...};
+}
+template <class St>
+static SqTable wave_tables(bool backward) {
+  return {wave_row<St, 1>(backward, SeqP{}), wave_row<St, 2>(backward, SeqP{}), wave_row<St, 3>(backward, SeqP{}),
+          wave_row<St, 4>(backward, SeqP{})};
+}
 
 template <class St>
 BcaStoreTables make_store_tables() {
-  return {fwd_row<St>(SeqP{}), bwd_row<St>(SeqP{}), sq_fwd_tables<St>(), sq_bwd_tables<St>()};
+  return {fwd_row<St>(SeqP{}),      bwd_row<St>(SeqP{}),     sq_fwd_tables<St>(),
+          sq_bwd_tables<St>(),      wave_tables<St>(false), wave_tables<St>(true)};
 }
 
 BcaStoreTables bca_tables_f32();
