@@ -47,6 +47,7 @@ ROWS = 1 << 16
 BCA = dict(tokens=4096, d=4096, p=1024, sigma=0.01)
 POOL_BYTES = 1 << 30
 PROBE_STEPS = 3
+SPIN_CYCLES = 3_000_000  # a GPU spin long enough (~1.5 ms) for the host to queue a table row's calls
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 
 
@@ -197,17 +198,26 @@ def config_table(dev, stream, reps: int = 10):
     (bf16, 2^16 rows each), forward and inverse, each over a rotating >= 1 GiB pool;
     and the four layer shapes (256-wide p = 64, fp32, 128 tokens; 768-wide p = 256,
     4096-wide p = 1024, 8192-wide p = 8192, bf16, 4096 tokens) and one 65536-wide circulant
-    (p = 65536, bf16, 1024 tokens; the multi-pass layer) forward and backward.  GB/s are algorithmic bytes over the
-    event-timed average of `reps` back-to-back calls; frac is of 8 TB/s.
+    (p = 65536, bf16, 1024 tokens; the multi-pass layer) forward and backward; and the
+    encoder-style configuration as a whole step (24 instances of the 768-wide layer).  GB/s
+    are algorithmic bytes over the event-timed average of `reps` back-to-back calls, queued
+    behind a GPU spin so that the host's launch rate does not enter; frac is of 8 TB/s.
     """
     import torch
 
     from paper_2511_01385_amd import api
 
+    def queue_behind_spin():
+        # the GPU spins while the timed calls are queued, so that the events time the GPU's
+        # work rather than the host's launch rate (short calls launch slower than they run)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(SPIN_CYCLES)
+
     def timed(fn, args_list):
         for a in args_list[:2]:
             fn(*a)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        queue_behind_spin()
         e0.record(stream)
         for i in range(reps):
             fn(*args_list[i % len(args_list)])
@@ -230,6 +240,7 @@ def config_table(dev, stream, reps: int = 10):
         for b in pool[:1]:
             api.rdfft_forward(b)
             api.rdfft_inverse(b)
+        queue_behind_spin()
         e0.record(stream)
         for i in range(reps_n):
             api.rdfft_forward(pool[i % len(pool)])
@@ -269,7 +280,49 @@ def config_table(dev, stream, reps: int = 10):
             "forward_GB_s": round(bf / us_f / 1e3, 1), "backward_GB_s": round(bb / us_b / 1e3, 1)}
         del sets
     torch.cuda.empty_cache()
+    table["bca_encoder_step_bf16_d768_p256_T4096_x24"] = encoder_step(dev, stream, queue_behind_spin)
     return table
+
+
+def encoder_step(dev, stream, queue_behind_spin, reps: int = 5):
+    """The encoder-style configuration as one step: forward and backward of the 768-wide
+    p = 256 bf16 layer (4096 tokens) for 24 instances, the query and value projections of
+    12 layers, each with its own x, y, gy, dx, spectra and dc (every instance's forward,
+    then every instance's backward).  Algorithmic bytes per instance: forward x, y and the
+    spectra; backward x, gy, dx, the spectra and dc."""
+    import torch
+
+    from paper_2511_01385_amd import api
+
+    T, d, p, n_inst = 4096, 768, 256, 24
+    q = kb = d // p
+    insts = [dict(x=torch.randn(T, d, device=dev).to(torch.bfloat16),
+                  c=(0.02 * torch.randn(q, kb, p, device=dev)).to(torch.bfloat16),
+                  g=torch.randn(T, d, device=dev).to(torch.bfloat16),
+                  y=torch.empty(T, d, device=dev, dtype=torch.bfloat16),
+                  dx=torch.empty(T, d, device=dev, dtype=torch.bfloat16),
+                  dc=torch.empty(q, kb, p, device=dev)) for _ in range(n_inst)]
+
+    def step():
+        for st in insts:
+            api.bca_forward(st["x"], st["c"], st["y"])
+        for st in insts:
+            api.bca_backward(st["x"], st["c"], st["g"], st["dx"], st["dc"])
+
+    step()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    queue_behind_spin()
+    e0.record(stream)
+    for _ in range(reps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    nbytes = n_inst * ((2 * T * d * 2 + q * kb * p * 2) + (3 * T * d * 2 + q * kb * p * 2 + q * kb * p * 4))
+    del insts
+    torch.cuda.empty_cache()
+    return {"instances": n_inst, "step_us": round(us, 2), "GB_s": round(nbytes / us / 1e3, 1),
+            "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "bytes_per_step": nbytes}
 
 
 def copy_rate(dev, stream, reps: int = 5):
