@@ -26,10 +26,11 @@ struct AtomicAddF32 {  // a time-domain row of dc, added into
 
 // threads of the finish kernel: a row of more than 64 threads synchronises with workgroup
 // barriers, so the workgroup is that one row; shorter rows synchronise at wave level only,
-// and the workgroup keeps the row kernels' size, its other threads helping with the sums
+// and the workgroup has one thread per slot (at least 64, at most 1024) for the sums
 template <int LOGN>
 constexpr int finish_wg() {
-  return RowPlan<LOGN>::TPR > 64 ? RowPlan<LOGN>::TPR : RowPlan<LOGN>::WG;
+  constexpr int N = RowPlan<LOGN>::N;
+  return RowPlan<LOGN>::TPR > 64 ? RowPlan<LOGN>::TPR : (N < 64 ? 64 : (N > 1024 ? 1024 : N));
 }
 
 template <int LOGN>
@@ -49,9 +50,18 @@ __global__ void __launch_bounds__(finish_wg<LOGN>()) bca_dc_finish_kernel(const 
     const int e = ij * N + k;
     const int ch = e / chunk;
     const float2* p = stage + ((int64_t)ch * groups + b0) * tile_f2 + (e - ch * chunk);
-    float2 v = make_float2(0.f, 0.f);
-#pragma unroll 8
-    for (int b = b0; b < b1; ++b, p += tile_f2) v = c_add(v, *p);
+    // all of a full group's loads in flight at once
+    float2 part[kReduceGroup];
+    if (b1 - b0 == kReduceGroup) {
+      static_for<kReduceGroup>([&](auto bc) { part[decltype(bc)::value] = p[decltype(bc)::value * tile_f2]; });
+    } else {
+      for (int b = 0; b < kReduceGroup; ++b) {
+        part[b] = make_float2(0.f, 0.f);
+        if (b < b1 - b0) part[b] = p[b * tile_f2];
+      }
+    }
+    float2 v = part[0];
+    static_for<kReduceGroup - 1>([&](auto bc) { v = c_add(v, part[decltype(bc)::value + 1]); });
     reg[lds_pad(k)] = v;
   }
   __syncthreads();
