@@ -227,6 +227,35 @@ def test_f16_layers(shape):
     _check(x, c, g, "f16", d_out, p, got, f"f16 {shape}", sampled=sampled)
 
 
+# square layers with blocks of 128 ... 512 (the wave kernels): every block count they take, token
+# counts that leave a partial last group, that stage the dC sums (every workgroup's first groups
+# whole) or add them with atomics, and dx over gy; shapes past their limits fall back to the
+# square kernels (p = 256 with 4 x 4 blocks backward, p = 512 with 3 x 3 blocks)
+WAVE = [
+    (37, 128, 128, "bf16", False),
+    (21, 256, 128, "f32", False),
+    (13, 384, 128, "bf16", True),
+    (9, 512, 128, "f16", False),
+    (4104, 512, 128, "bf16", False),
+    (11, 256, 256, "f32", True),
+    (4099, 768, 256, "bf16", False),
+    (4100, 768, 256, "f16", True),
+    (333, 1024, 256, "bf16", False),
+    (29, 512, 512, "bf16", False),
+    (2048, 1024, 512, "f32", False),
+    (2053, 1024, 512, "bf16", True),
+    (19, 1536, 512, "bf16", False),
+]
+
+
+@pytest.mark.parametrize("shape", WAVE, ids=[f"T{s[0]}_{s[1]}_p{s[2]}_{s[3]}{'_aliased' if s[4] else ''}" for s in WAVE])
+def test_wave_kernel_layers(shape):
+    tokens, d, p, dtype, alias = shape
+    x, c, g = _problem(3131 + tokens, tokens, d, d, p, 0.05, dtype)
+    got = _run(x, c, g, dtype, d, alias_dx=alias)
+    _check(x, c, g, dtype, d, p, got, f"wave {shape}")
+
+
 # square layers whose dC slots exceed LDS, with dx == gy: the dC launches read gy, so they
 # must all run before the dx launch overwrites it
 SPLIT_ALIASED = [(5, 4096, 128, "bf16"), (3, 4096, 512, "f32"), (4, 4096, 512, "bf16"), (3, 8192, 1024, "bf16")]
