@@ -80,7 +80,7 @@ typedef enum {
  *         Theorem 1); any other even n -> RDFFT_EUNSUPPORTED.
  * No memory beyond buf is read or written (apart from the twiddle table).
  */
-RDFFT_API int rdfft_forward(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);
+RDFFT_API int rdfft_forward(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
 
 /*
  * rdfft_inverse -- in-place inverse of rdfft_forward (Sec. 4.2; Sec. 3.1
@@ -89,7 +89,7 @@ RDFFT_API int rdfft_forward(void *buf, int64_t rows, int64_t n, int dtype, rdfft
  * with the imaginary parts of Y_0 and Y_{n/2} taken as zero.  Any n reals are
  * a valid packed spectrum.  Arguments and errors as rdfft_forward.
  */
-RDFFT_API int rdfft_inverse(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);
+RDFFT_API int rdfft_inverse(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
 
 /*
  * rdfft_pairs_to_halfcomplex / rdfft_halfcomplex_to_pairs -- in-place change of
@@ -103,8 +103,8 @@ RDFFT_API int rdfft_inverse(void *buf, int64_t rows, int64_t n, int dtype, rdfft
  * converted to halfcomplex must be converted back before it is inverted.
  * Arguments and errors as rdfft_forward.
  */
-RDFFT_API int rdfft_pairs_to_halfcomplex(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);
-RDFFT_API int rdfft_halfcomplex_to_pairs(void *buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream);
+RDFFT_API int rdfft_pairs_to_halfcomplex(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
+RDFFT_API int rdfft_halfcomplex_to_pairs(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
 
 /* Gradient outputs of bca_backward. */
 typedef struct {
@@ -136,7 +136,7 @@ typedef struct {
  * staged spectra are stored in dtype (for 16-bit storage one more rounding of each spectrum).
  */
 RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_grads_t *grads, int64_t d_in,
-                int64_t d_out, int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream);
+                int64_t d_out, int64_t p, int64_t tokens, rdfft_dtype_t dtype, rdfft_stream_t stream);
 
 /*
  * bca_backward -- gradients of the block-circulant layer (Sec. 3.3, Eq. (5)):
@@ -158,7 +158,7 @@ RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_gra
  * Any other overlap between the buffers -> RDFFT_EINVAL.
  */
 RDFFT_API int bca_backward(const void *x, const void *c_spectra, void *gy, bca_grads_t *grads, int64_t d_in,
-                 int64_t d_out, int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream);
+                 int64_t d_out, int64_t p, int64_t tokens, rdfft_dtype_t dtype, rdfft_stream_t stream);
 
 /* Uploads the twiddle table to the current device (synchronously) if not done yet.
  * Optional: every entry point does it on first use.  Returns RDFFT_OK or RDFFT_EDEVICE. */

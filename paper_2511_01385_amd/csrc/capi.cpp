@@ -154,24 +154,24 @@ int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t
 
 extern "C" {
 
-int rdfft_forward(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+int rdfft_forward(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
   return transform(buf, rows, n, dtype, stream, false);
 }
 
-int rdfft_inverse(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+int rdfft_inverse(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
   return transform(buf, rows, n, dtype, stream, true);
 }
 
-int rdfft_pairs_to_halfcomplex(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+int rdfft_pairs_to_halfcomplex(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
   return convert(buf, rows, n, dtype, stream, true);
 }
 
-int rdfft_halfcomplex_to_pairs(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream) {
+int rdfft_halfcomplex_to_pairs(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
   return convert(buf, rows, n, dtype, stream, false);
 }
 
 int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grads, int64_t d_in, int64_t d_out,
-                int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream) {
+                int64_t p, int64_t tokens, rdfft_dtype_t dtype, rdfft_stream_t stream) {
   if (grads != nullptr) return RDFFT_EINVAL;
   BcaShape sh;
   int st = check_bca(x, c_spectra, y, d_in, d_out, p, tokens, dtype, false, &sh);
@@ -194,7 +194,7 @@ int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grad
 }
 
 int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* grads, int64_t d_in, int64_t d_out,
-                 int64_t p, int64_t tokens, int dtype, rdfft_stream_t stream) {
+                 int64_t p, int64_t tokens, rdfft_dtype_t dtype, rdfft_stream_t stream) {
   if (grads == nullptr) return RDFFT_EINVAL;
   BcaShape sh;
   int st = check_bca(x, c_spectra, gy, d_in, d_out, p, tokens, dtype, true, &sh);

@@ -169,3 +169,35 @@ def test_bca_backward_long_blocks_need_separate_dx(lib):
 
 def test_bca_backward_needs_grads(lib):
     assert lib.bca_backward(A, B, G, None, 256, 256, 64, 8, F32, None) == EINVAL
+
+
+def test_header_compiles_as_c_and_links(tmp_path):
+    """include/rdfft.h is plain C: a C99 program built with gcc against it links with the library and
+    gets the documented answers for calls that never reach a device (empty inputs, validation)."""
+    src = tmp_path / "abi.c"
+    src.write_text(r'''
+#include <stdio.h>
+#include <string.h>
+#include "rdfft.h"
+int main(void) {
+  rdfft_dtype_t dt = RDFFT_BF16;
+  if (rdfft_forward(NULL, 0, 4096, dt, NULL) != RDFFT_OK) return 1;       /* no rows: a no-op */
+  if (rdfft_inverse(NULL, 0, 96, RDFFT_F16, NULL) != RDFFT_OK) return 2;  /* mixed radix, no rows */
+  if (rdfft_forward(NULL, 4, 14, RDFFT_F32, NULL) != RDFFT_EUNSUPPORTED) return 3;  /* n/2 = 7 */
+  if (rdfft_forward(NULL, 4, 64, (rdfft_dtype_t)7, NULL) != RDFFT_EINVAL) return 4;
+  bca_grads_t g = {NULL, NULL};
+  if (bca_backward(NULL, NULL, NULL, &g, 256, 256, 64, 8, RDFFT_F32, NULL) != RDFFT_EINVAL) return 5;
+  if (bca_forward(NULL, NULL, NULL, NULL, 256, 256, 96, 8, RDFFT_F32, NULL) != RDFFT_EINVAL) return 6;
+  if (strncmp(rdfft_status_string(RDFFT_OK), "RDFFT_OK", 8) != 0) return 7;
+  if (rdfft_table_bytes() <= 0) return 8;
+  printf("ok\n");
+  return 0;
+}
+''')
+    exe = tmp_path / "abi"
+    libdir = os.path.dirname(_lib.LIB_PATH)
+    cmd = ["gcc", "-std=c99", "-Wall", "-Werror", f"-I{os.path.join(ROOT, 'include')}", str(src), "-o", str(exe),
+           f"-L{libdir}", "-lrdfft", f"-Wl,-rpath,{libdir}"]
+    subprocess.run(cmd, check=True, capture_output=True, text=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and r.stdout.strip() == "ok", (r.returncode, r.stdout, r.stderr)
