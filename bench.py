@@ -196,7 +196,9 @@ def config_table(dev, stream, reps: int = 10):
     Batched transforms for each n in 64..4096 (2^16 rows) in fp32 and bf16 storage,
     n = 65536 (1024 rows, fp32) and the mixed-radix lengths n = 3000 (fp32) and n = 6144
     (bf16, 2^16 rows each), forward and inverse, each over a rotating >= 1 GiB pool;
-    and the four layer shapes (256-wide p = 64, fp32, 128 tokens; 768-wide p = 256,
+    (the forward of one pool slot, then the inverse of a slot made spectral half a pool
+    earlier: pair_us and frac from the pairs timed as one block, forward_us / inverse_us
+    from a pass with every call between its own events); and the four layer shapes (256-wide p = 64, fp32, 128 tokens; 768-wide p = 256,
     4096-wide p = 1024, 8192-wide p = 8192, bf16, 4096 tokens) and one 65536-wide circulant
     (p = 65536, bf16, 1024 tokens; the multi-pass layer) forward and backward; and the
     encoder-style configuration as a whole step (24 instances of the 768-wide layer).  GB/s
@@ -233,29 +235,50 @@ def config_table(dev, stream, reps: int = 10):
         tdt = torch.float32 if dt == "f32" else torch.bfloat16
         nb = rows * n * (4 if dt == "f32" else 2)
         pool = [torch.randn(rows, n, device=dev).to(tdt) for _ in range(max(2, -(-POOL_BYTES // nb)))]
-        # forwards over the whole pool, then inverses in the same order: every buffer
-        # returns to its input and no call finds its data in the Infinity Cache
-        reps_n = len(pool) * ((reps + len(pool) - 1) // len(pool))
-        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-        for b in pool[:1]:
-            api.rdfft_forward(b)
-            api.rdfft_inverse(b)
-        queue_behind_spin()
-        e0.record(stream)
-        for i in range(reps_n):
-            api.rdfft_forward(pool[i % len(pool)])
-        e1.record(stream)
-        for i in range(reps_n):
-            api.rdfft_inverse(pool[i % len(pool)])
-        e2.record(stream)
-        torch.cuda.synchronize()
-        us_f = e0.elapsed_time(e1) * 1e3 / reps_n
-        us_i = e1.elapsed_time(e2) * 1e3 / reps_n
+        # alternating, as in the bench step: the forward of slot i, then the inverse of slot
+        # i - h, made spectral h forwards earlier (>= 0.5 GiB of traffic ago, so not read from
+        # the Infinity Cache).  A block of forwards followed by a block of inverses would time
+        # the second block at a lower engine clock (sustained load), whichever direction it
+        # holds.  The pairs are timed as one block (pair_us, which gives GB/s and frac); a
+        # second pass brackets every call with its own events for the split between the
+        # directions, which then includes each launch's start-up (~2 us).
+        P = len(pool)
+        h = max(1, P // 2)
+        reps_n = P * ((reps + P - 1) // P)
+
+        def pairs(ev):
+            for j in range(P - h, P):
+                api.rdfft_forward(pool[j])
+            queue_behind_spin()
+            if ev is None:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            for i in range(reps_n):
+                for k, (fn, buf) in enumerate(((api.rdfft_forward, pool[i % P]), (api.rdfft_inverse, pool[(i - h) % P]))):
+                    if ev is not None:
+                        ev[2 * i + k][0].record(stream)
+                    fn(buf)
+                    if ev is not None:
+                        ev[2 * i + k][1].record(stream)
+            if ev is None:
+                e1.record(stream)
+            for i in range(reps_n, reps_n + h):  # every slot back to its input
+                api.rdfft_inverse(pool[(i - h) % P])
+            torch.cuda.synchronize()
+            return None if ev is not None else e0.elapsed_time(e1) * 1e3 / reps_n
+
+        pair_us = pairs(None)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(2 * reps_n)]
+        pairs(ev)
+        us_f = float(np.mean([a.elapsed_time(b) for a, b in ev[0::2]])) * 1e3
+        us_i = float(np.mean([a.elapsed_time(b) for a, b in ev[1::2]])) * 1e3
         gbs_f, gbs_i = 2 * nb / us_f / 1e3, 2 * nb / us_i / 1e3
+        gbs_pair = 4 * nb / pair_us / 1e3
         table[f"rdfft_{dt}_n{n}_rows{rows}"] = {
+            "pair_us": round(pair_us, 2), "GB_s": round(gbs_pair, 1),
             "forward_us": round(us_f, 2), "inverse_us": round(us_i, 2),
             "forward_GB_s": round(gbs_f, 1), "inverse_GB_s": round(gbs_i, 1),
-            "frac": round((gbs_f + gbs_i) / 2 / HBM_PEAK_GBS, 4)}
+            "frac": round(gbs_pair / HBM_PEAK_GBS, 4)}
         del pool
     torch.cuda.empty_cache()
     # the paper's four layer shapes (the 256-wide one in fp32), then one circulant beyond the
