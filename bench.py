@@ -194,8 +194,9 @@ def config_table(dev, stream, reps: int = 10):
     """Untimed-by-`value` context: every workload shape of the paper's configurations.
 
     Batched transforms for each n in 64..4096 (2^16 rows) in fp32 and bf16 storage,
-    n = 65536 (1024 rows, fp32) and the mixed-radix lengths n = 3000 (fp32) and n = 6144
-    (bf16, 2^16 rows each), forward and inverse, each over a rotating >= 1 GiB pool;
+    n = 65536 (1024 rows, fp32), the mixed-radix lengths n = 3000 (fp32) and n = 6144
+    (bf16, 2^16 rows each) and n = 4096 in the halfcomplex layout (bf16), forward and
+    inverse, each over a rotating >= 1 GiB pool;
     (the forward of one pool slot, then the inverse of a slot made spectral half a pool
     earlier: pair_us and frac from the pairs timed as one block, forward_us / inverse_us
     from a pass with every call between its own events); and the four layer shapes (256-wide p = 64, fp32, 128 tokens; 768-wide p = 256,
@@ -229,9 +230,13 @@ def config_table(dev, stream, reps: int = 10):
 
     table = {}
     # the batched-transform sizes, the longest rows, and two mixed-radix lengths
-    shapes = [(n, ROWS, dt) for dt in ("f32", "bf16") for n in NS] + [(65536, 1024, "f32")]
-    shapes += [(3000, ROWS, "f32"), (6144, ROWS, "bf16")]
-    for n, rows, dt in shapes:
+    shapes = [(n, ROWS, dt, "") for dt in ("f32", "bf16") for n in NS] + [(65536, 1024, "f32", "")]
+    shapes += [(3000, ROWS, "f32", ""), (6144, ROWS, "bf16", "")]
+    # the transforms with the spectrum in the halfcomplex layout, at the largest batched size
+    shapes += [(4096, ROWS, "bf16", "hc_")]
+    for n, rows, dt, lay in shapes:
+        fwd, inv = ((api.rdfft_forward_halfcomplex, api.rdfft_inverse_halfcomplex) if lay
+                    else (api.rdfft_forward, api.rdfft_inverse))
         tdt = torch.float32 if dt == "f32" else torch.bfloat16
         nb = rows * n * (4 if dt == "f32" else 2)
         pool = [torch.randn(rows, n, device=dev).to(tdt) for _ in range(max(2, -(-POOL_BYTES // nb)))]
@@ -248,13 +253,13 @@ def config_table(dev, stream, reps: int = 10):
 
         def pairs(ev):
             for j in range(P - h, P):
-                api.rdfft_forward(pool[j])
+                fwd(pool[j])
             queue_behind_spin()
             if ev is None:
                 e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                 e0.record(stream)
             for i in range(reps_n):
-                for k, (fn, buf) in enumerate(((api.rdfft_forward, pool[i % P]), (api.rdfft_inverse, pool[(i - h) % P]))):
+                for k, (fn, buf) in enumerate(((fwd, pool[i % P]), (inv, pool[(i - h) % P]))):
                     if ev is not None:
                         ev[2 * i + k][0].record(stream)
                     fn(buf)
@@ -263,7 +268,7 @@ def config_table(dev, stream, reps: int = 10):
             if ev is None:
                 e1.record(stream)
             for i in range(reps_n, reps_n + h):  # every slot back to its input
-                api.rdfft_inverse(pool[(i - h) % P])
+                inv(pool[(i - h) % P])
             torch.cuda.synchronize()
             return None if ev is not None else e0.elapsed_time(e1) * 1e3 / reps_n
 
@@ -274,7 +279,7 @@ def config_table(dev, stream, reps: int = 10):
         us_i = float(np.mean([a.elapsed_time(b) for a, b in ev[1::2]])) * 1e3
         gbs_f, gbs_i = 2 * nb / us_f / 1e3, 2 * nb / us_i / 1e3
         gbs_pair = 4 * nb / pair_us / 1e3
-        table[f"rdfft_{dt}_n{n}_rows{rows}"] = {
+        table[f"rdfft_{lay}{dt}_n{n}_rows{rows}"] = {
             "pair_us": round(pair_us, 2), "GB_s": round(gbs_pair, 1),
             "forward_us": round(us_f, 2), "inverse_us": round(us_i, 2),
             "forward_GB_s": round(gbs_f, 1), "inverse_GB_s": round(gbs_i, 1),

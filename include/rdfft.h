@@ -100,11 +100,24 @@ RDFFT_API int rdfft_inverse(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dt
  * (so pair slot k, i.e. elements 2k and 2k+1, maps to elements k and n-k, and
  * pair slot 0 to elements 0 and n/2).  Values are moved bit for bit; NaN
  * payloads included.  rdfft_inverse expects the pairs layout, so a spectrum
- * converted to halfcomplex must be converted back before it is inverted.
+ * converted to halfcomplex must be converted back before it is inverted (or
+ * inverted with rdfft_inverse_halfcomplex).
  * Arguments and errors as rdfft_forward.
  */
 RDFFT_API int rdfft_pairs_to_halfcomplex(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
 RDFFT_API int rdfft_halfcomplex_to_pairs(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
+
+/*
+ * rdfft_forward_halfcomplex / rdfft_inverse_halfcomplex -- the in-place transforms
+ * with the spectrum in the halfcomplex layout above (Sec. 4.1, Memory Layout) instead
+ * of pairs: the forward leaves Re Y_k at element k and Im Y_k at element n-k, the
+ * inverse reads them from there.  The results equal rdfft_forward followed by
+ * rdfft_pairs_to_halfcomplex (and rdfft_halfcomplex_to_pairs followed by
+ * rdfft_inverse) bit for bit, in one pass over the data instead of two.  Arguments
+ * and errors as rdfft_forward.
+ */
+RDFFT_API int rdfft_forward_halfcomplex(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
+RDFFT_API int rdfft_inverse_halfcomplex(void *buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream);
 
 /* Gradient outputs of bca_backward. */
 typedef struct {

@@ -27,6 +27,8 @@ EXPORTS = (
     "rdfft_inverse",
     "rdfft_pairs_to_halfcomplex",
     "rdfft_halfcomplex_to_pairs",
+    "rdfft_forward_halfcomplex",
+    "rdfft_inverse_halfcomplex",
     "bca_forward",
     "bca_backward",
     "rdfft_init",
@@ -52,7 +54,8 @@ def load() -> ctypes.CDLL:
         raise ImportError(f"{LIB_PATH} is not built; run paper_2511_01385_amd.build.build() first")
     lib = ctypes.CDLL(LIB_PATH)
     vp, i64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int
-    for name in ("rdfft_forward", "rdfft_inverse", "rdfft_pairs_to_halfcomplex", "rdfft_halfcomplex_to_pairs"):
+    for name in ("rdfft_forward", "rdfft_inverse", "rdfft_pairs_to_halfcomplex", "rdfft_halfcomplex_to_pairs",
+                 "rdfft_forward_halfcomplex", "rdfft_inverse_halfcomplex"):
         f = getattr(lib, name)
         f.argtypes = [vp, i64, i64, i32, vp]
         f.restype = i32

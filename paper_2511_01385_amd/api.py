@@ -66,6 +66,24 @@ def rdfft_inverse(buf: torch.Tensor) -> torch.Tensor:
     return buf
 
 
+def rdfft_forward_halfcomplex(buf: torch.Tensor) -> torch.Tensor:
+    """In place: each row becomes its packed spectrum in the halfcomplex layout.  Returns ``buf``."""
+    n = buf.shape[-1]
+    rows = buf.numel() // n if n else 0
+    st = _lib.load().rdfft_forward_halfcomplex(_dev(buf, "buf"), rows, n, _code(buf), _stream(buf))
+    _check(st, "rdfft_forward_halfcomplex")
+    return buf
+
+
+def rdfft_inverse_halfcomplex(buf: torch.Tensor) -> torch.Tensor:
+    """In place: each halfcomplex-layout spectrum row becomes its real signal.  Returns ``buf``."""
+    n = buf.shape[-1]
+    rows = buf.numel() // n if n else 0
+    st = _lib.load().rdfft_inverse_halfcomplex(_dev(buf, "buf"), rows, n, _code(buf), _stream(buf))
+    _check(st, "rdfft_inverse_halfcomplex")
+    return buf
+
+
 def rdfft_pairs_to_halfcomplex(buf: torch.Tensor) -> torch.Tensor:
     """In place: each packed spectrum row moves from the pairs to the halfcomplex layout."""
     n = buf.shape[-1]

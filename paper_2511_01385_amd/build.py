@@ -19,7 +19,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "librdfft.so")
 
-SOURCES = ["bca_store_bf16.hip", "bca_store_f16.hip", "bca_store_f32.hip", "rdfft_kernels.hip", "bca_kernels.hip", "bca_multipass.hip", "layout_kernels.hip", "mixed_kernels.hip", "capi.cpp", "twiddles.cpp"]
+SOURCES = ["bca_store_bf16.hip", "bca_store_f16.hip", "bca_store_f32.hip", "rdfft_kernels.hip", "rdfft_hc_kernels.hip", "bca_kernels.hip", "bca_multipass.hip", "layout_kernels.hip", "mixed_kernels.hip", "capi.cpp", "twiddles.cpp"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

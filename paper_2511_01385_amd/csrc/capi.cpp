@@ -92,7 +92,8 @@ int check_transform(const void* buf, int64_t rows, int64_t n, int dtype) {
   return RDFFT_OK;
 }
 
-int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream, bool inv) {
+// hc: the spectrum side of the transform in the halfcomplex layout instead of pairs
+int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stream, bool inv, bool hc) {
   int st = check_transform(buf, rows, n, dtype);
   if (st != RDFFT_OK || rows == 0) return st;
   const float2* tw = nullptr;
@@ -100,8 +101,10 @@ int transform(void* buf, int64_t rows, int64_t n, int dtype, rdfft_stream_t stre
   st = ensure_device(&tw, &num_cu);
   if (st != RDFFT_OK) return st;
   const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const hipError_t e = is_pow2(n) ? rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype, inv, tw, s, num_cu)
-                                  : rdfft::launch_mixed_rows(buf, rows, n, dtype, inv, s);
+  hipError_t e;
+  if (!is_pow2(n)) e = rdfft::launch_mixed_rows(buf, rows, n, dtype, inv, hc, s);
+  else if (hc) e = rdfft::launch_rdfft_rows_hc(buf, rows, ilog2(n) - 1, dtype, inv, tw, s);
+  else e = rdfft::launch_rdfft_rows(buf, rows, ilog2(n) - 1, dtype, inv, tw, s, num_cu);
   return e == hipSuccess ? RDFFT_OK : RDFFT_ELAUNCH;
 }
 
@@ -155,11 +158,19 @@ int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t
 extern "C" {
 
 int rdfft_forward(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
-  return transform(buf, rows, n, dtype, stream, false);
+  return transform(buf, rows, n, dtype, stream, false, false);
 }
 
 int rdfft_inverse(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
-  return transform(buf, rows, n, dtype, stream, true);
+  return transform(buf, rows, n, dtype, stream, true, false);
+}
+
+int rdfft_forward_halfcomplex(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
+  return transform(buf, rows, n, dtype, stream, false, true);
+}
+
+int rdfft_inverse_halfcomplex(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {
+  return transform(buf, rows, n, dtype, stream, true, true);
 }
 
 int rdfft_pairs_to_halfcomplex(void* buf, int64_t rows, int64_t n, rdfft_dtype_t dtype, rdfft_stream_t stream) {

@@ -244,6 +244,51 @@ struct ConstF16 {
   __device__ __forceinline__ float2 load(int m) const { return f16x2_to_f32(base[m]); }
 };
 
+// A row's packed spectrum in the halfcomplex layout (Sec. 4.1, Memory Layout): Re Y_k at
+// real slot k (0 <= k <= N) and Im Y_k at real slot 2N - k (1 <= k < N).  Pair slot m of the
+// pairs layout is thus the two real slots (m, 2N - m), and pair slot 0 = (Y_0, Y_{n/2}) the
+// slots (0, N).  G is the row's pairs accessor (GlobalF32, GlobalBF16 or GlobalF16), which
+// gives a pair's storage form; every pair is read and written as two scalars.
+template <class G>
+struct Halfcomplex {
+  using raw_t = typename G::raw_t;
+  static constexpr bool kF32 = std::is_same<raw_t, float2>::value;
+  using scalar_t = typename std::conditional<kF32, float, uint16_t>::type;
+  scalar_t* base;  // real slot 0 of the row
+  int N;           // pair slots per row (n / 2)
+  __device__ __forceinline__ int partner(int m) const { return m == 0 ? N : 2 * N - m; }
+  __device__ __forceinline__ static float2 widen(raw_t r) { return G::widen(r); }
+  __device__ __forceinline__ raw_t load_raw(int m) const {
+    const scalar_t a = base[m], b = base[partner(m)];
+    if constexpr (kF32) {
+      return make_float2(a, b);
+    } else {
+      return (uint32_t)a | ((uint32_t)b << 16);
+    }
+  }
+  __device__ __forceinline__ float2 load(int m) const { return widen(load_raw(m)); }
+  __device__ __forceinline__ void store(int m, float2 v) const {
+    const raw_t r = G::narrow(v);
+    if constexpr (kF32) {
+      base[m] = r.x;
+      base[partner(m)] = r.y;
+    } else {
+      base[m] = (uint16_t)(r & 0xffffu);
+      base[partner(m)] = (uint16_t)(r >> 16);
+    }
+  }
+};
+
+// The spectrum side of a row at p (n = 2N reals): halfcomplex (HC) or pairs.
+template <bool HC, class G, class Elem>
+__device__ __forceinline__ auto spectrum_view(Elem* p, int N) {
+  if constexpr (HC) {
+    return Halfcomplex<G>{reinterpret_cast<typename Halfcomplex<G>::scalar_t*>(p), N};
+  } else {
+    return G{p};
+  }
+}
+
 // Storage types of the layer kernels: the pair type in memory (Elem), its read-only and
 // read-write row accessors, and the value of rdfft_dtype_t it stands for.  bf16 and f16
 // share the 32-bit pair type, so the layer kernels are instantiated per storage struct.

@@ -21,6 +21,10 @@ constexpr int64_t kMaxGridThreads = (int64_t)1 << 31;
 // (rows >= 1) stored as `storage`.
 hipError_t launch_rdfft_rows(void* buf, int64_t rows, int logn, int storage, bool inv, const float2* tw,
                              hipStream_t stream, int num_cu);
+// The same transforms with the spectrum in the halfcomplex layout (the forward's output,
+// the inverse's input).
+hipError_t launch_rdfft_rows_hc(void* buf, int64_t rows, int logn, int storage, bool inv, const float2* tw,
+                                hipStream_t stream);
 
 // In-place conversion of `rows` packed spectra of 2^(logn+1) elements between the pairs
 // layout and the halfcomplex layout (rows >= 1); half16 = 16-bit storage (bf16 or f16).
@@ -31,7 +35,8 @@ hipError_t launch_layout_convert(void* buf, int64_t rows, int logn, bool half16,
 // (mixed_kernels.hip): the transforms and the layout converters, rows >= 1.
 constexpr int64_t kMixedMaxHalf = 16384;
 bool mixed_length_supported(int64_t n);
-hipError_t launch_mixed_rows(void* buf, int64_t rows, int64_t n, int storage, bool inv, hipStream_t stream);
+hipError_t launch_mixed_rows(void* buf, int64_t rows, int64_t n, int storage, bool inv, bool halfcomplex,
+                             hipStream_t stream);
 hipError_t launch_mixed_layout(void* buf, int64_t rows, int64_t n, bool half16, bool to_halfcomplex,
                                hipStream_t stream);
 

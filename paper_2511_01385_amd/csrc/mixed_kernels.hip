@@ -143,24 +143,27 @@ __device__ __forceinline__ void mixed_passes(float2* lds, const MixedPlan& plan)
   }
 }
 
-template <class Acc, class Elem, bool INV>
+// HC: the spectrum (the forward's output, the inverse's input) in the halfcomplex layout.
+template <class Acc, class Elem, bool INV, bool HC>
 __global__ void __launch_bounds__(1024) mixed_rows_kernel(Elem* buf, MixedPlan plan) {
   extern __shared__ float2 mixed_lds[];
   const int N = plan.n_half, T = blockDim.x, t = threadIdx.x;
-  const Acc row{buf + (int64_t)blockIdx.x * N};
+  Elem* const rp = buf + (int64_t)blockIdx.x * N;
+  const Acc sig{rp};                                   // the signal pairs (x_{2m}, x_{2m+1})
+  const auto spec = spectrum_view<HC, Acc>(rp, N);  // the packed spectrum
   if constexpr (!INV) {
-    for (int m = t; m < N; m += T) mixed_lds[m] = row.load(m);
+    for (int m = t; m < N; m += T) mixed_lds[m] = sig.load(m);
   } else {
     // pre-pass: Z~_m = (s + i conj(W_n^m) d) / n, Z~_{N-m} = conj(s - i conj(W_n^m) d) / n with
     // s = Y_m + conj(Y_{N-m}), d = Y_m - conj(Y_{N-m}); slot 0 holds (Y_0, Y_{n/2})
     const float sc = 1.0f / (2.0f * N);
     for (int m = t; 2 * m <= N; m += T) {
-      const float2 ya = row.load(m);
+      const float2 ya = spec.load(m);
       if (m == 0) {
         mixed_lds[0] = make_float2(sc * (ya.x + ya.y), sc * (ya.x - ya.y));
         continue;
       }
-      const float2 yb = c_conj(row.load(N - m));
+      const float2 yb = c_conj(spec.load(N - m));
       const float2 s = c_add(ya, yb), d = c_sub(ya, yb);
       const float2 w = unit_root_dev<true>(m, 2 * N);         // conj(W_n^m)
       const float2 q = c_mul<false>(d, make_float2(-sc * w.y, sc * w.x));  // i conj(W_n^m) d / n
@@ -176,18 +179,18 @@ __global__ void __launch_bounds__(1024) mixed_rows_kernel(Elem* buf, MixedPlan p
     for (int k = t; 2 * k <= N; k += T) {
       const float2 a = mixed_lds[k];
       if (k == 0) {
-        row.store(0, make_float2(a.x + a.y, a.x - a.y));
+        spec.store(0, make_float2(a.x + a.y, a.x - a.y));
         continue;
       }
       const float2 b = c_conj(mixed_lds[N - k]);
       const float2 s = c_add(a, b), d = c_sub(a, b);
       const float2 w = unit_root_dev<false>(k, 2 * N);  // W_n^k
       const float2 q = c_mul<false>(d, make_float2(0.5f * w.y, -0.5f * w.x));  // -i W_n^k d / 2
-      row.store(k, make_float2(fmaf(s.x, 0.5f, q.x), fmaf(s.y, 0.5f, q.y)));
-      if (2 * k != N) row.store(N - k, make_float2(fmaf(s.x, 0.5f, -q.x), -fmaf(s.y, 0.5f, -q.y)));
+      spec.store(k, make_float2(fmaf(s.x, 0.5f, q.x), fmaf(s.y, 0.5f, q.y)));
+      if (2 * k != N) spec.store(N - k, make_float2(fmaf(s.x, 0.5f, -q.x), -fmaf(s.y, 0.5f, -q.y)));
     }
   } else {
-    for (int m = t; m < N; m += T) row.store(m, mixed_lds[m]);
+    for (int m = t; m < N; m += T) sig.store(m, mixed_lds[m]);
   }
 }
 
@@ -197,16 +200,16 @@ hipError_t allow_lds(K kernel) {
                              160 * 1024);
 }
 
-template <class Acc, class Elem, bool INV>
+template <class Acc, class Elem, bool INV, bool HC>
 hipError_t launch_mixed(void* buf, int64_t rows, const MixedPlan& plan, int threads, hipStream_t stream) {
-  static const hipError_t attr = allow_lds(mixed_rows_kernel<Acc, Elem, INV>);
+  static const hipError_t attr = allow_lds(mixed_rows_kernel<Acc, Elem, INV, HC>);
   if (attr != hipSuccess) return attr;
   const size_t lds = (size_t)plan.n_half * sizeof(float2);
   Elem* base = static_cast<Elem*>(buf);
   const int64_t max_rows = kMaxGridThreads / threads;
   for (int64_t r0 = 0; r0 < rows; r0 += max_rows) {
     const int64_t nr = std::min<int64_t>(max_rows, rows - r0);
-    hipLaunchKernelGGL((mixed_rows_kernel<Acc, Elem, INV>), dim3((unsigned)nr), dim3(threads), lds, stream,
+    hipLaunchKernelGGL((mixed_rows_kernel<Acc, Elem, INV, HC>), dim3((unsigned)nr), dim3(threads), lds, stream,
                        base + r0 * plan.n_half, plan);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -304,16 +307,20 @@ bool mixed_length_supported(int64_t n) {
   return n % 2 == 0 && make_plan(n / 2, &p);
 }
 
-hipError_t launch_mixed_rows(void* buf, int64_t rows, int64_t n, int storage, bool inv, hipStream_t stream) {
+hipError_t launch_mixed_rows(void* buf, int64_t rows, int64_t n, int storage, bool inv, bool halfcomplex,
+                             hipStream_t stream) {
   MixedPlan plan;
   if (!make_plan(n / 2, &plan)) return hipErrorInvalidValue;
   const int threads = threads_for(n / 2);
   using Fn = hipError_t (*)(void*, int64_t, const MixedPlan&, int, hipStream_t);
-  static const Fn table[3][2] = {
-      {&launch_mixed<GlobalF32, float2, false>, &launch_mixed<GlobalF32, float2, true>},
-      {&launch_mixed<GlobalBF16, uint32_t, false>, &launch_mixed<GlobalBF16, uint32_t, true>},
-      {&launch_mixed<GlobalF16, uint32_t, false>, &launch_mixed<GlobalF16, uint32_t, true>}};
-  return table[storage][inv ? 1 : 0](buf, rows, plan, threads, stream);
+  static const Fn table[2][3][2] = {
+      {{&launch_mixed<GlobalF32, float2, false, false>, &launch_mixed<GlobalF32, float2, true, false>},
+       {&launch_mixed<GlobalBF16, uint32_t, false, false>, &launch_mixed<GlobalBF16, uint32_t, true, false>},
+       {&launch_mixed<GlobalF16, uint32_t, false, false>, &launch_mixed<GlobalF16, uint32_t, true, false>}},
+      {{&launch_mixed<GlobalF32, float2, false, true>, &launch_mixed<GlobalF32, float2, true, true>},
+       {&launch_mixed<GlobalBF16, uint32_t, false, true>, &launch_mixed<GlobalBF16, uint32_t, true, true>},
+       {&launch_mixed<GlobalF16, uint32_t, false, true>, &launch_mixed<GlobalF16, uint32_t, true, true>}}};
+  return table[halfcomplex ? 1 : 0][storage][inv ? 1 : 0](buf, rows, plan, threads, stream);
 }
 
 }  // namespace rdfft
