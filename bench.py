@@ -301,10 +301,12 @@ def config_table(dev, stream, reps: int = 10):
                      dc=torch.empty(q, kb, p, device=dev)) for _ in range(nset)]
         us_f = timed(lambda st: api.bca_forward(st["x"], st["c"], st["y"]), [(st,) for st in sets])
         us_b = timed(lambda st: api.bca_backward(st["x"], st["c"], st["g"], st["dx"], st["dc"]), [(st,) for st in sets])
+        # the in-place backward (dx over gy, Sec. 5.1.1): same bytes, gy rewritten in place
+        us_bi = timed(lambda st: api.bca_backward(st["x"], st["c"], st["g"], st["g"], st["dc"]), [(st,) for st in sets])
         bf = 2 * T * d * s + q * kb * p * s
         bb = 3 * T * d * s + q * kb * p * s + q * kb * p * 4
         table[f"bca_{dt}_d{d}_p{p}_T{T}"] = {
-            "forward_us": round(us_f, 2), "backward_us": round(us_b, 2),
+            "forward_us": round(us_f, 2), "backward_us": round(us_b, 2), "backward_inplace_us": round(us_bi, 2),
             "forward_GB_s": round(bf / us_f / 1e3, 1), "backward_GB_s": round(bb / us_b / 1e3, 1)}
         del sets
     torch.cuda.empty_cache()

@@ -144,9 +144,12 @@ typedef struct {
  *   p          power of two, 2 <= p <= 65536 (larger -> RDFFT_EUNSUPPORTED);
  *              must divide d_in and d_out (Table 1 marks such shapes N/A) -> else RDFFT_EINVAL.
  *   tokens     >= 0; 0 is a no-op (x and y may then be NULL).
- * Blocks beyond 8192 (p = 16384, 32768, 65536) run as passes over HBM that stage the
- * input spectra in y: they need kb <= q and kb <= 8 (else RDFFT_EUNSUPPORTED), and the
- * staged spectra are stored in dtype (for 16-bit storage one more rounding of each spectrum).
+ * Blocks beyond 8192 (p = 16384, 32768, 65536) run as passes over HBM with q * kb <= 65535
+ * (else RDFFT_EUNSUPPORTED).  With kb <= q and kb <= 8 they stage the input spectra in y;
+ * other shapes add each input block's contribution into y's spectra, one pass per block.
+ * Either way the intermediate spectra are stored in dtype (for 16-bit storage, one more
+ * rounding of each staged spectrum, or of each of the kb partial sums).  In place
+ * (y == x) they need q = kb <= 8 (else RDFFT_EUNSUPPORTED).
  */
 RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_grads_t *grads, int64_t d_in,
                 int64_t d_out, int64_t p, int64_t tokens, rdfft_dtype_t dtype, rdfft_stream_t stream);
@@ -161,10 +164,10 @@ RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_gra
  *   gy         [tokens][d_out] in dtype: the upstream gradient.  Its contents
  *              are unspecified on return (the layer may use it as work space,
  *              Sec. 5.1.1 "overwriting the grad_output").
- *   grads->dx  [tokens][d_in] in dtype, written; may equal gy when d_in == d_out and
- *              p <= 8192.  Blocks beyond 8192 stage the input spectra in dx while gy
- *              holds the upstream ones: dx == gy -> RDFFT_EUNSUPPORTED, and q * kb must
- *              not exceed 65535.
+ *   grads->dx  [tokens][d_in] in dtype, written; may equal gy when d_in == d_out.
+ *              Blocks beyond 8192 stage the input spectra in dx while gy holds the
+ *              upstream ones; with dx == gy (q = kb <= 8 there, else RDFFT_EUNSUPPORTED)
+ *              each token's input spectra go straight into float32 atomic sums of dc.
  *   grads->dc  [q][kb][p] float32, written (overwritten, not accumulated).
  *              Summed with float32 atomics, so the last bits may vary run to run.
  *   Other arguments as bca_forward.  tokens == 0 writes dc = 0.

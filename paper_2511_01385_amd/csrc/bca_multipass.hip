@@ -4,16 +4,24 @@
 // The steps of Eqs. (4)-(5) run as separate passes over HBM.  The intermediate spectra
 // live in the caller's own output buffers, so the layer still needs no memory beyond
 // them:
-//   forward   X_tj = FFT(x_tj) into y's segment j (needs kb <= q), then per bin
-//             Y_ti = sum_j C_ij X_tj in place, then y_ti = IFFT(Y_ti) in place.  A single
-//             circulant (q == kb == 1) instead runs both transforms and the product in
-//             one row kernel, the spectrum staying in registers (p <= 32768), or takes
-//             the product as the inverse loads (p = 65536).
+//   forward   X_tj = FFT(x_tj) into y's segment j (when kb <= q and kb <= 8), then per
+//             bin Y_ti = sum_j C_ij X_tj in place, then y_ti = IFFT(Y_ti) in place.
+//             Other shapes (y distinct from x) take one pass per input block j instead:
+//             the transform of x_tj hands each bin of X_tj to the store, which adds
+//             C_ij X_tj into every Y_ti in y (the first pass writes), so no input
+//             spectrum is staged; then y_ti = IFFT(Y_ti).  A single circulant
+//             (q == kb == 1) runs both transforms and the product in one row kernel, the
+//             spectrum staying in registers (p <= 32768), or takes the product as the
+//             inverse loads (p = 65536).
 //   backward  G_ti = FFT(g_ti) in place in gy; X_tj = FFT(x_tj) into dx; per bin
 //             dC_ij = sum_t conj(X_tj) G_ti (float32 atomics into dc); per bin
 //             dX_tj = sum_i conj(C_ij) G_ti into dx; dx_tj = IFFT(dX_tj) in place; the
 //             caller's dc rows are then inverted like the fused path's.  With
 //             q == kb == 1 the dx product is applied as the inverse loads.
+//             When dx is gy (Sec. 5.1.1, overwriting the grad_output; q == kb <= 8)
+//             there is nowhere to stage X: its transform hands each bin to the store,
+//             which adds conj(X_tj) G_ti into dc_ij for every i (float32 atomics), and
+//             dX_tj then replaces G_tj per bin in place in gy.
 // The intermediate spectra are stored in the layer's storage type (the in-place
 // transform keeps a spectrum in the storage of its input, Sec. 4.1); the arithmetic is
 // float32 throughout.
@@ -28,7 +36,7 @@ namespace {
 
 constexpr int kMpMinLogN = 13;  // p = 16384
 constexpr int kMpMaxLogN = 15;  // p = 65536
-constexpr int kMpMaxKb = 8;     // forward: input blocks held per bin
+constexpr int kMpMaxKb = kMpMaxInPlaceBlocks;  // blocks a per-bin product thread holds
 
 // elementwise product of pair slot m with the matching slot of a spectrum w (times
 // conj(w) when CONJ); slot 0 holds the two real bins Y_0 and Y_{n/2}
@@ -76,6 +84,83 @@ __global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, St>()>::WG))
   const typename S::In in{src + row * (int64_t)P::N};
   const typename S::Out out{dst + out_row * (int64_t)P::N};
   row_forward<LOGN, false, typename S::In, typename S::Out, CH>(t, true, in, out, lds, tw);
+}
+
+// Post-pass destinations that consume a spectrum bin by bin instead of storing it.
+// YAccumulate: the bins of X_tj (token t, input block j) add C_ij X_tj into Y_ti for
+// every output block i, in y's segments (stored in the layer's storage type; `first`
+// writes instead of adding).
+template <class St>
+struct YAccumulate {
+  ElemOf<St>* y;             // Y_t0
+  const ElemOf<St>* c;       // C_0j
+  int q;
+  int64_t n_slots, cstride;  // pair slots per row; between C_ij and C_(i+1)j
+  bool first;
+  __device__ __forceinline__ void store(int m, float2 xv) const {
+    for (int i = 0; i < q; ++i) {
+      float2 v = slot_mul<false>(m, xv, St::In::widen(c[i * cstride + m]));
+      ElemOf<St>* yp = y + i * n_slots + m;
+      if (!first) v = c_add(v, St::Out::widen(*yp));
+      *yp = St::Out::narrow(v);
+    }
+  }
+};
+
+// DcAccumulate: the bins of X_tj add conj(X_tj) G_ti into dc_ij (float32 atomics) for
+// every output block i, G_ti being the upstream spectra in gy.
+template <class St>
+struct DcAccumulate {
+  const ElemOf<St>* g;        // G_t0
+  float* dc;                  // dc_0j, float32 pairs
+  int q;
+  int64_t n_slots, dcstride;  // pair slots per row; between dc_ij and dc_(i+1)j
+  __device__ __forceinline__ void store(int m, float2 xv) const {
+    for (int i = 0; i < q; ++i) {
+      const float2 v = slot_mul<true>(m, St::In::widen(g[i * n_slots + m]), xv);  // G . conj(X)
+      float* d = dc + 2 * (i * dcstride + m);
+      unsafeAtomicAdd(d, v.x);
+      unsafeAtomicAdd(d + 1, v.y);
+    }
+  }
+};
+
+// Forward pass for input block j of every token: row t of the grid transforms x_tj and
+// adds C_ij X_tj into y_t's output segments.  One launch per j, in order.
+template <int LOGN, class St>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, St>()>::WG))
+    mp_fwd_accumulate_kernel(const ElemOf<St>* x, ElemOf<St>* y, const ElemOf<St>* c, int64_t tokens, int q, int kb,
+                             int j, const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, St>();
+  using P = RowPlan<LOGN, CH>;
+  static_assert(P::RW == 1, "one row per workgroup");
+  __shared__ float2 lds[P::LDS_F2];
+  const int64_t tok = blockIdx.x;
+  if (tok >= tokens) return;  // whole workgroup
+  constexpr int64_t N = P::N;
+  const typename St::In in{x + (tok * kb + j) * N};
+  const YAccumulate<St> acc{y + tok * q * N, c + (int64_t)j * N, q, N, (int64_t)kb * N, j == 0};
+  row_forward<LOGN, false, typename St::In, YAccumulate<St>, CH>(threadIdx.x, true, in, acc, lds, tw);
+}
+
+// dC for the in-place backward: row r = t*kb + j of the grid transforms x_tj and adds
+// conj(X_tj) G_ti into dc_ij for every i.
+template <int LOGN, class St>
+__global__ void __launch_bounds__((RowPlan<LOGN, mp_chunks<LOGN, St>()>::WG))
+    mp_dc_accumulate_kernel(const ElemOf<St>* x, const ElemOf<St>* g, float* dc, int64_t rows, int q, int kb,
+                            const float2* __restrict__ tw) {
+  constexpr int CH = mp_chunks<LOGN, St>();
+  using P = RowPlan<LOGN, CH>;
+  static_assert(P::RW == 1, "one row per workgroup");
+  __shared__ float2 lds[P::LDS_F2];
+  const int64_t row = blockIdx.x;
+  if (row >= rows) return;  // whole workgroup
+  constexpr int64_t N = P::N;
+  const int64_t tok = row / kb;
+  const int j = (int)(row - tok * kb);
+  const typename St::In in{x + row * N};
+  const DcAccumulate<St> acc{g + tok * q * N, dc + 2 * (int64_t)j * N, q, N, (int64_t)kb * N};
+  row_forward<LOGN, false, typename St::In, DcAccumulate<St>, CH>(threadIdx.x, true, in, acc, lds, tw);
 }
 
 // dst row r = IFFT(spec . src row r), or IFFT(conj(spec) . src row r) when CONJ: the
@@ -194,6 +279,30 @@ __global__ void __launch_bounds__(256) mp_dx_product_kernel(const ElemOf<St>* g,
   dx[row * nslots + m] = St::Out::narrow(acc);
 }
 
+// In place in gy (dx == gy, q == kb): per bin, dX_tj = sum_i conj(C_ij) G_ti replaces G_tj.
+// One thread owns slot m of one token across all segments, so it reads every G_ti[m]
+// before it writes any dX_tj[m].
+template <class St>
+__global__ void __launch_bounds__(256) mp_dx_inplace_kernel(ElemOf<St>* g, const ElemOf<St>* c, int64_t tokens, int q,
+                                                            int nslots, int xblocks) {
+  const int64_t b = blockIdx.x;
+  const int64_t tok = b / xblocks;
+  const int m = (int)(b - tok * xblocks) * 256 + threadIdx.x;
+  if (tok >= tokens || m >= nslots) return;
+  ElemOf<St>* gt = g + tok * (int64_t)q * nslots;
+  float2 gv[kMpMaxKb];
+#pragma unroll
+  for (int i = 0; i < kMpMaxKb; ++i)
+    if (i < q) gv[i] = St::Out::widen(gt[(int64_t)i * nslots + m]);
+  for (int j = 0; j < q; ++j) {
+    float2 acc = make_float2(0.f, 0.f);
+#pragma unroll
+    for (int i = 0; i < kMpMaxKb; ++i)
+      if (i < q) acc = c_add(acc, slot_mul<true>(m, gv[i], St::Out::widen(c[((int64_t)i * q + j) * nslots + m])));
+    gt[(int64_t)j * nslots + m] = St::Out::narrow(acc);
+  }
+}
+
 // dC_ij[m] += sum_{t in chunk} conj(X_tj[m]) G_ti[m]; grid (slot blocks, q*kb, chunks).
 template <class St>
 __global__ void __launch_bounds__(256) mp_dc_kernel(const ElemOf<St>* xs, const ElemOf<St>* g, float* dc, int64_t tokens, int q,
@@ -298,6 +407,24 @@ hipError_t mp_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, in
   if constexpr (LOGN < kMpMaxLogN) {
     if (a.q == 1 && a.kb == 1) return circulant_rows<LOGN, St>(a.x, a.y, a.c, xrows, tw, stream);
   }
+  if (a.kb > a.q || a.kb > kMpMaxKb) {
+    // no room to stage the input spectra in y: one accumulating pass per input block
+    if (a.x == a.y) return hipErrorInvalidValue;  // in place needs q == kb <= kMpMaxKb
+    using P = RowPlan<LOGN, mp_chunks<LOGN, St>()>;
+    const int64_t per_launch = kMaxGridThreads / P::WG;
+    for (int j = 0; j < a.kb; ++j) {
+      for (int64_t t0 = 0; t0 < a.tokens; t0 += per_launch) {
+        const int64_t nt = std::min<int64_t>(per_launch, a.tokens - t0);
+        hipLaunchKernelGGL((mp_fwd_accumulate_kernel<LOGN, St>), dim3((unsigned)nt), dim3(P::WG), 0, stream,
+                           static_cast<const ElemOf<St>*>(a.x) + t0 * a.kb * (int64_t)N,
+                           static_cast<ElemOf<St>*>(a.y) + t0 * a.q * (int64_t)N, static_cast<const ElemOf<St>*>(a.c), nt,
+                           a.q, a.kb, j, tw);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+      }
+    }
+    return launch_rdfft_rows(a.y, a.tokens * a.q, LOGN, storage, true, tw, stream, num_cu);
+  }
   hipError_t e = forward_rows<LOGN, St>(a.x, a.y, xrows, a.kb, a.q, tw, stream);
   if (e != hipSuccess) return e;
   if (a.q == 1 && a.kb == 1) return inverse_mul_rows<LOGN, St, false>(a.y, a.y, a.c, xrows, tw, stream);
@@ -316,13 +443,40 @@ hipError_t mp_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, i
   constexpr int N = 1 << LOGN;
   constexpr int storage = St::kId;
   const int64_t grows = a.tokens * a.q, xrows = a.tokens * a.kb;
-  // G = FFT(g) in place; X = FFT(x) into dx
+  // G = FFT(g) in place
   hipError_t e = launch_rdfft_rows(a.y, grows, LOGN, storage, false, tw, stream, num_cu);
   if (e != hipSuccess) return e;
+  const int xblocks = (N + 255) / 256;
+  if (a.dx == a.y) {
+    // in place (q == kb <= kMpMaxKb): dC from the transforms of x as they complete, then
+    // dX per bin over G, then its inverse
+    if (a.q != a.kb || a.q > kMpMaxKb) return hipErrorInvalidValue;
+    using P = RowPlan<LOGN, mp_chunks<LOGN, St>()>;
+    const int64_t per_launch = kMaxGridThreads / P::WG;
+    for (int64_t r0 = 0; r0 < xrows;) {
+      // launches start at whole tokens
+      const int64_t nr = std::min<int64_t>((per_launch / a.kb) * a.kb, xrows - r0);
+      const int64_t t0 = r0 / a.kb;
+      hipLaunchKernelGGL((mp_dc_accumulate_kernel<LOGN, St>), dim3((unsigned)nr), dim3(P::WG), 0, stream,
+                         static_cast<const ElemOf<St>*>(a.x) + r0 * (int64_t)N,
+                         static_cast<const ElemOf<St>*>(a.y) + t0 * a.q * (int64_t)N, a.dc, nr, a.q, a.kb, tw);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      r0 += nr;
+    }
+    if (a.q == 1) return inverse_mul_rows<LOGN, St, true>(a.y, a.y, a.c, xrows, tw, stream);
+    ElemOf<St>* g = static_cast<ElemOf<St>*>(a.y);
+    e = per_row_slots(a.tokens, xblocks, [&](int64_t t0, int64_t nt, unsigned blocks) {
+      hipLaunchKernelGGL(mp_dx_inplace_kernel<St>, dim3(blocks), dim3(256), 0, stream, g + t0 * a.q * (int64_t)N,
+                         static_cast<const ElemOf<St>*>(a.c), nt, a.q, N, xblocks);
+    });
+    if (e != hipSuccess) return e;
+    return launch_rdfft_rows(a.y, xrows, LOGN, storage, true, tw, stream, num_cu);
+  }
+  // X = FFT(x) into dx
   e = forward_rows<LOGN, St>(a.x, a.dx, xrows, 1, 1, tw, stream);
   if (e != hipSuccess) return e;
   // dC: slot blocks x pairs x token chunks, about 2048 workgroups in all (q * kb <= 65535)
-  const int xblocks = (N + 255) / 256;
   const int pairs = a.q * a.kb;
   int64_t chunks = std::max<int64_t>(1, 2048 / ((int64_t)xblocks * pairs));
   chunks = std::min<int64_t>(chunks, std::max<int64_t>(1, a.tokens / 16));
@@ -356,12 +510,10 @@ MpRow mp_row(bool backward, std::integer_sequence<int, L...>) {
 
 }  // namespace
 
-bool bca_multipass_supported(int logp, int q, int kb, bool backward) {
+bool bca_multipass_supported(int logp, int q, int kb, bool) {
   const int logn = logp - 1;
   if (logn < kMpMinLogN || logn > kMpMaxLogN) return false;
-  if ((int64_t)q * kb > 65535) return false;  // the dC grid's second dimension
-  if (backward) return true;
-  return kb <= q && kb <= kMpMaxKb;
+  return (int64_t)q * kb <= 65535;  // the dC grid's second dimension
 }
 
 hipError_t launch_bca_circulant(const BcaArgs& a, const float2* tw, hipStream_t stream) {

@@ -191,6 +191,7 @@ int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grad
   // y may be x itself (an in-place layer) only when the shapes agree
   if (y == x) {
     if (d_in != d_out) return RDFFT_EINVAL;
+    if (p > 8192 && sh.q > rdfft::kMpMaxInPlaceBlocks) return RDFFT_EUNSUPPORTED;
   } else if (overlaps(x, sh.x_bytes, y, sh.y_bytes)) {
     return RDFFT_EINVAL;
   }
@@ -220,8 +221,7 @@ int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* gr
     if (overlaps(dx, sh.x_bytes, x, sh.x_bytes) || overlaps(dx, sh.x_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
     if (dx == gy) {
       if (d_in != d_out) return RDFFT_EINVAL;
-      // blocks beyond 8192 stage the input spectra in dx while gy holds the upstream ones
-      if (p > 8192) return RDFFT_EUNSUPPORTED;
+      if (p > 8192 && sh.q > rdfft::kMpMaxInPlaceBlocks) return RDFFT_EUNSUPPORTED;
     } else if (overlaps(dx, sh.x_bytes, gy, sh.y_bytes)) {
       return RDFFT_EINVAL;
     }

@@ -61,10 +61,11 @@ hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t s
 // whether the fused forward (or backward) kernel handles p = 2^logp with q x kb blocks
 bool bca_shape_supported(int logp, int q, int kb, bool backward);
 
-// The multi-pass layer for 8192 < p <= 65536 (bca_multipass.hip).  The forward needs
-// kb <= q (the input spectra are staged in y); the backward needs dx distinct from gy
-// (the input spectra are staged in dx while gy holds the upstream spectra).  The
-// backward launcher expects dc zeroed and leaves it as packed spectra.
+// The multi-pass layer for 8192 < p <= 65536 (bca_multipass.hip), q * kb <= 65535.  In
+// place (y == x in the forward, dx == gy in the backward, so q == kb) it takes at most
+// kMpMaxInPlaceBlocks blocks: a per-bin product holds that many values.  The backward
+// launcher expects dc zeroed and leaves it as packed spectra.
+constexpr int kMpMaxInPlaceBlocks = 8;
 bool bca_multipass_supported(int logp, int q, int kb, bool backward);
 // The forward of a single circulant (q == kb == 1) of p = 2^(kCirculantLogN+1) = 8192 as
 // one row kernel per token (bca_multipass.hip), the spectrum handed from the forward to

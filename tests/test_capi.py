@@ -110,8 +110,8 @@ def _grads(dx, dc):
         (A, B, A + (1 << 29), 256, 192, 128, 8, F32, EINVAL),  # p does not divide d_out
         (A, B, A + (1 << 29), 96, 96, 48, 8, F32, EUNSUP),  # even, not a power of two
         (A, B, A + (1 << 29), 131072, 131072, 131072, 8, F32, EUNSUP),  # p beyond 65536
-        (A, B, A + (1 << 29), 32768, 16384, 16384, 8, F32, EUNSUP),  # long blocks, kb > q
-        (A, B, A + (1 << 29), 147456, 147456, 16384, 8, F32, EUNSUP),  # long blocks, kb > 8
+        (A, B, A, 147456, 147456, 16384, 8, F32, EUNSUP),  # long blocks in place, q = kb > 8
+        (A, B, A + (1 << 29), 4194304, 4194304, 16384, 1, F32, EUNSUP),  # long blocks, q * kb > 65535
         (A, B, A + (1 << 29), 256, 256, 7, 8, F32, EINVAL),  # odd p
         (A, B, A + (1 << 29), 256, 256, 64, -1, F32, EINVAL),
         (A, B, A + (1 << 29), 0, 256, 64, 8, F32, EINVAL),
@@ -162,9 +162,9 @@ def test_bca_backward_validation(lib, x, gy, dx, dc, d_in, d_out, want):
     assert lib.bca_backward(x, B, gy, _grads(dx, dc), d_in, d_out, 64, 8, F32, None) == want
 
 
-def test_bca_backward_long_blocks_need_separate_dx(lib):
-    # blocks beyond 8192 stage the input spectra in dx while gy holds the upstream ones
-    assert lib.bca_backward(A, B, G, _grads(G, DC), 16384, 16384, 16384, 8, F32, None) == EUNSUP
+def test_bca_backward_long_blocks_in_place_at_most_eight_blocks(lib):
+    # in place (dx == gy) beyond 8192, a per-bin product holds at most 8 blocks
+    assert lib.bca_backward(A, B, G, _grads(G, DC), 147456, 147456, 16384, 8, F32, None) == EUNSUP
 
 
 def test_bca_backward_needs_grads(lib):

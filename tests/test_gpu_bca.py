@@ -97,12 +97,13 @@ def _dc_bar(dtype, p):
 SAMPLE_RTOL = {"f32": 1e-4, "bf16": 2e-2, "f16": 2e-3}
 
 
-def _check(x, c, g, dtype, d_out, p, got, what, sampled=0):
+def _check(x, c, g, dtype, d_out, p, got, what, sampled=0, y_staged=None):
     y, dx, dc = got
     x64, c64, g64 = inputs.to_f64(x, dtype), inputs.to_f64(c, dtype), inputs.to_f64(g, dtype)
     q, kb = c.shape[0], c.shape[1]
     staged = 2 if p > 8192 else 0  # spectra stored on the way (storage type)
-    assert_close(y, obca.forward_spectral(x64, c64, d_out, p), dtype, f"{what} y", staged)
+    assert_close(y, obca.forward_spectral(x64, c64, d_out, p), dtype, f"{what} y",
+                 staged if y_staged is None else y_staged)
     rdx, rdc = obca.backward_spectral(x64, c64, g64, p)
     assert_close(dx, rdx, dtype, f"{what} dx", staged)
     assert_close(dc.reshape(q * kb, p), rdc.reshape(q * kb, p), _dc_bar(dtype, p), f"{what} dc", staged)
@@ -176,16 +177,69 @@ def test_long_blocks(shape):
 @pytest.mark.parametrize("d", [16384, 32768])
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_long_blocks_in_place_forward(dtype, d):
-    """y may be x for long blocks too (a single circulant, and 2 x 2 blocks); dx must then
-    be its own buffer (not gy)."""
+    """y may be x for long blocks too (a single circulant, and 2 x 2 blocks)."""
     tokens, p = 3, 16384
     x, c, g = _problem(77, tokens, d, d, p, 0.004, dtype)
     got = _run(x, c, g, dtype, d, alias_y=True)
     _check(x, c, g, dtype, d, p, got, "long aliased y")
-    xt, ct, gt = to_device(x, dtype), to_device(c, dtype), to_device(g, dtype)
-    dct = torch.empty(c.shape, dtype=torch.float32, device="cuda")
+
+
+# blocks beyond 8192 whose input spectra do not fit y's segments (kb > q) or a per-bin
+# thread (kb > 8): one accumulating pass per input block; a 16-bit y then holds kb
+# rounded partial sums of its spectrum on the way
+LONG_ACCUMULATE = [
+    (3, 32768, 16384, 16384, "bf16"),  # q = 1, kb = 2
+    (2, 49152, 32768, 16384, "f32"),  # q = 2, kb = 3
+    (2, 147456, 147456, 16384, "f32"),  # q = kb = 9
+    (3, 131072, 65536, 65536, "bf16"),  # q = 1, kb = 2
+    (2, 98304, 32768, 32768, "f32"),  # q = 1, kb = 3
+]
+
+
+@pytest.mark.parametrize("shape", LONG_ACCUMULATE, ids=[f"T{s[0]}_{s[1]}x{s[2]}_p{s[3]}_{s[4]}"
+                                                        for s in LONG_ACCUMULATE])
+def test_long_blocks_accumulating_forward(shape):
+    tokens, d_in, d_out, p, dtype = shape
+    x, c, g = _problem(6161 + tokens, tokens, d_in, d_out, p, 0.004, dtype)
+    got = _run(x, c, g, dtype, d_out)
+    _check(x, c, g, dtype, d_out, p, got, str(shape), sampled=5, y_staged=d_in // p + 1)
+
+
+# the in-place backward for blocks beyond 8192 (dx == gy, Sec. 5.1.1): dC from the input
+# transforms as they complete (float32 atomics), dX per bin over G in gy
+LONG_ALIASED = [
+    (3, 16384, 16384, "f32"),
+    (5, 16384, 16384, "bf16"),
+    (3, 32768, 16384, "bf16"),  # q = kb = 2
+    (2, 131072, 16384, "f32"),  # q = kb = 8
+    (4, 32768, 32768, "f32"),
+    (2, 65536, 65536, "f32"),
+    (2, 65536, 65536, "bf16"),
+    (19, 65536, 32768, "bf16"),  # q = kb = 2, more tokens
+]
+
+
+@pytest.mark.parametrize("shape", LONG_ALIASED, ids=[f"T{s[0]}_{s[1]}_p{s[2]}_{s[3]}" for s in LONG_ALIASED])
+def test_long_blocks_dx_over_gy(shape):
+    tokens, d, p, dtype = shape
+    x, c, g = _problem(7171 + tokens, tokens, d, d, p, 0.004, dtype)
+    got = _run(x, c, g, dtype, d, alias_dx=True)
+    _check(x, c, g, dtype, d, p, got, f"{shape} dx over gy", sampled=7)
+    got = _run(x, c, g, dtype, d, alias_y=True, alias_dx=True)
+    _check(x, c, g, dtype, d, p, got, f"{shape} y over x, dx over gy")
+
+
+def test_long_blocks_in_place_beyond_eight_blocks_unsupported():
+    """In place, a per-bin product holds at most 8 blocks: q = kb = 9 is refused before any launch."""
+    tokens, d, p = 1, 147456, 16384
+    x = torch.zeros((tokens, d), device="cuda")
+    c = torch.zeros((9, 9, p), device="cuda")
+    dc = torch.empty((9, 9, p), device="cuda")
     with pytest.raises(api.RdfftError):
-        api.bca_backward(xt, ct, gt, gt, dct)
+        api.bca_forward(x, c, x)
+    g = x.clone()
+    with pytest.raises(api.RdfftError):
+        api.bca_backward(x, c, g, g, dc)
 
 
 # square layers with enough tokens for the two-stage dC sum (dx apart from gy); 2048 bf16
