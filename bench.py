@@ -80,7 +80,8 @@ def source_digest() -> str:
     return h.hexdigest()[:16]
 
 
-def stored_traffic(kernel: str, digest: str):
+def stored_record(kernel: str, digest: str):
+    """The counter readings kept for a launch (profiles/traffic.json), if taken of these sources."""
     path = os.path.join(PROFILE_DIR, "traffic.json")
     if not os.path.exists(path):
         return None
@@ -89,7 +90,28 @@ def stored_traffic(kernel: str, digest: str):
     rec = data.get(kernel)
     if not rec or rec.get("source_digest") != digest:
         return None
-    return rec.get("bytes_per_launch")
+    return rec
+
+
+def stored_traffic(kernel: str, digest: str):
+    rec = stored_record(kernel, digest)
+    return rec.get("bytes_per_launch") if rec else None
+
+
+# VALU issue: one wave64 instruction per cycle per CU (four SIMDs, four cycles each; packed
+# FP32 forms, which would double the FP32 rate, are not used), at the peak engine clock
+VALU_CLOCK_GHZ = 2.4
+
+
+def valu_issue(kernel: str, digest: str, avg_us: float, num_cu: int):
+    """The dominant launch's VALU instruction count (SQ_INSTS_VALU per dispatch, stored with
+    its counters) against the time the CUs need just to issue them."""
+    rec = stored_record(kernel, digest)
+    if not rec or not rec.get("valu_insts"):
+        return None
+    bound_us = rec["valu_insts"] / (num_cu * VALU_CLOCK_GHZ * 1e3)
+    return {"insts_per_launch": rec["valu_insts"], "issue_bound_us": round(bound_us, 2),
+            "frac": round(bound_us / avg_us, 4), "clock_ghz": VALU_CLOCK_GHZ, "cus": num_cu}
 
 
 # float64 inputs of the CPU baseline, set before its worker processes fork so that they
@@ -533,6 +555,7 @@ def main():
         "launches_timed": len(events[dominant]),
         "algorithmic_bytes_per_launch": dom["bytes"],
     }
+    num_cu = torch.cuda.get_device_properties(0).multi_processor_count
     value = step_bytes * args.steps / wall / 1e9
     out = {
         "metric": METRIC,
@@ -556,6 +579,7 @@ def main():
             "bytes_per_step": step_bytes,
         },
         "hbm_fraction": round(value / HBM_PEAK_GBS, 4),
+        "valu_issue": valu_issue(dominant, digest, dom["avg_us"], num_cu),
         "aux_bytes": int(aux),
         "table_bytes": api.rdfft_table_bytes(),
         "roofline": roofline,
