@@ -11,7 +11,8 @@ buffers, casts the parameter and reshapes.
 Memory: the forward keeps x and the packed spectra (q*kb*p storage elements) for the
 backward, nothing else.  The backward needs one buffer of the upstream gradient's size,
 which the library uses as work space and then fills with dx (allowed when
-d_in == d_out and p <= 8192; otherwise dx gets its own buffer).  With ``clobber_grad=True`` it works
+d_in == d_out, and for blocks longer than 8192 when there are at most 8 of them per
+row; otherwise dx gets its own buffer).  With ``clobber_grad=True`` it works
 in the upstream gradient tensor itself instead of a copy, as the paper does
 ("overwriting the grad_output", Sec. 5.1.1); only do that when nothing else reads
 that gradient afterwards.
@@ -49,9 +50,9 @@ class _BcaFunction(torch.autograd.Function):
             gy = gy.to(x2d.dtype)
         elif not ctx.clobber_grad:
             gy = gy.clone()  # the library overwrites it
-        # dx may share the work buffer when the layer is square and its blocks fit the
-        # fused kernels; longer blocks stage the input spectra in dx
-        dx = gy if q == kb and p <= 8192 else torch.empty_like(x2d)
+        # dx may share the work buffer when the layer is square (for blocks beyond 8192, when
+        # a per-bin product holds its q blocks)
+        dx = gy if q == kb and (p <= 8192 or q <= 8) else torch.empty_like(x2d)
         dc = torch.empty((q, kb, p), dtype=torch.float32, device=x2d.device)
         api.bca_backward(x2d, spectra, gy, dx, dc)
         return dx, dc, None, None
@@ -62,8 +63,7 @@ class BlockCirculantLinear(torch.nn.Module):
 
     x has shape (..., d_in) and the storage type ``dtype`` (bfloat16, float16 or float32); y has
     shape (..., d_out).  p must be a power of two with 2 <= p <= 65536 dividing d_in and
-    d_out; blocks longer than 8192 also need d_in <= d_out and d_in <= 8p (their forward
-    stages the input spectra in y).  c is initialised N(0, sigma^2) with sigma = d_in^-1/2
+    d_out; blocks longer than 8192 also need (d_in/p)(d_out/p) <= 65535.  c is initialised N(0, sigma^2) with sigma = d_in^-1/2
     unless given.
     """
 
@@ -76,8 +76,8 @@ class BlockCirculantLinear(torch.nn.Module):
             raise ValueError(f"p = {p} must divide d_in = {d_in} and d_out = {d_out}")
         if p > 65536:
             raise ValueError(f"p = {p} is beyond the largest supported block, 65536")
-        if p > 8192 and (d_in > d_out or d_in > 8 * p):
-            raise ValueError(f"blocks of p = {p} > 8192 need d_in <= d_out and d_in <= 8p")
+        if p > 8192 and (d_in // p) * (d_out // p) > 65535:
+            raise ValueError(f"blocks of p = {p} > 8192 need (d_in/p)(d_out/p) <= 65535")
         if dtype not in (torch.bfloat16, torch.float16, torch.float32):
             raise TypeError(f"storage type must be bfloat16, float16 or float32, got {dtype}")
         self.d_in, self.d_out, self.p = d_in, d_out, p

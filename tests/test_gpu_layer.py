@@ -30,6 +30,8 @@ LAYER_SHAPES = [(dt, *sh) for dt in ("f32", "bf16") for sh in
                 [(256, 256, 64, (3, 5)), (512, 1024, 128, (7,)), (768, 256, 256, (2, 3)), (4096, 4096, 512, (3,)),
                  (16384, 16384, 16384, (2, 2))]]
 LAYER_SHAPES += [("f16", 256, 256, 64, (3, 5)), ("f16", 768, 768, 256, (4, 3)), ("f16", 16384, 16384, 16384, (2, 2))]
+# blocks beyond 8192 with more input than output blocks (one accumulating forward pass per block)
+LAYER_SHAPES += [("f32", 32768, 16384, 16384, (3,)), ("bf16", 32768, 32768, 16384, (2, 2))]
 
 
 @pytest.mark.parametrize("dtype,d_in,d_out,p,lead", LAYER_SHAPES,

@@ -7,7 +7,7 @@ from paper_2511_01385_amd.layer import BlockCirculantLinear
 
 
 @pytest.mark.parametrize("d_in,d_out,p", [(256, 256, 48), (256, 256, 1), (256, 192, 128), (100, 100, 8),
-                                          (131072, 131072, 131072), (32768, 16384, 16384), (147456, 147456, 16384)])
+                                          (131072, 131072, 131072), (4194304, 4194304, 16384)])
 def test_rejects_bad_block_sizes(d_in, d_out, p):
     with pytest.raises(ValueError):
         BlockCirculantLinear(d_in, d_out, p, device="cpu")
