@@ -76,7 +76,7 @@ typedef enum {
  *   rows  >= 0; rows == 0 is a no-op (buf may then be NULL).
  *   n     even, 2 <= n: a power of two up to 65536, or n = 2N with N = 2^a 3^b 5^c
  *         up to 16384 (mixed-radix rows: one workgroup per row, the row in LDS,
- *         twiddles from sincospi).  Odd n -> RDFFT_EINVAL (no Nyquist bin,
+ *         twiddles from the hardware sine and cosine).  Odd n -> RDFFT_EINVAL (no Nyquist bin,
  *         Theorem 1); any other even n -> RDFFT_EUNSUPPORTED.
  * No memory beyond buf is read or written (apart from the twiddle table).
  */

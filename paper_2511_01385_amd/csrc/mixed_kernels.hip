@@ -5,9 +5,9 @@
 // z_m = x_{2m} + i x_{2m+1} followed by the post-pass that pairs bins k and N-k, and the
 // inverse pre-pass (1/n folded in) followed by the conjugate passes.  Here one workgroup
 // owns one row, keeps all N complex points in LDS, and runs a Stockham pass per radix
-// (5, 3, then 8/4/2) with the radix picked at run time; the twiddles come from sincospi
-// of the exact reduced fraction, and a butterfly's higher powers from products of its first
-// one, so these plans need no table.
+// (5, 3, then 8/4/2) with the radix picked at run time; the twiddles come from the
+// hardware sine and cosine of the fraction k/M in revolutions, and a butterfly's higher
+// powers from products of its first one, so these plans need no table.
 #include <hip/hip_runtime.h>
 
 #include "fft_device.hpp"
@@ -79,17 +79,24 @@ __device__ __forceinline__ void dft_any(float2* v) {
   else Dft<R, INV>::run(v);
 }
 
-// exp(-+ 2 pi i num / den) for 0 <= num < den: sincospi of the exact fraction
+// exp(-+ 2 pi i num / den) for 0 <= num < den, from the hardware sine and cosine of the
+// angle in revolutions, num / den (V_SIN_F32 / V_COS_F32 take their argument in turns, so
+// no reduction by pi is needed); the caller passes inv_den = 1/den (one division per pass,
+// not per twiddle).  Transform errors stay at 1e-7 .. 6e-7 relative (fp64 reference),
+// against 1e-7 .. 3e-7 with sincospif, whose argument reduction costs more instructions.
 template <bool INV>
-__device__ __forceinline__ float2 unit_root_dev(int num, int den) {
-  float s, c;
-  sincospif(2.0f * (float)num / (float)den, &s, &c);
+__device__ __forceinline__ float2 unit_root_dev(int num, float inv_den) {
+  const float x = (float)num * inv_den;  // revolutions
+  const float s = __builtin_amdgcn_sinf(x), c = __builtin_amdgcn_cosf(x);
   return make_float2(c, INV ? s : -s);
 }
 
 // One Stockham pass of radix R over the row in LDS: butterfly j < B = N/R reads
 // in[j + r*B], multiplies input r by W_{Ns*R}^{r*k} (k = j mod Ns), runs the R-point DFT
-// and writes out[(j/Ns)*Ns*R + k + r*Ns].  All reads of the pass precede its writes.
+// and writes out[(j/Ns)*Ns*R + k + r*Ns].  All reads of the pass precede its writes.  A
+// thread's butterflies are T apart, so their k follow from the first one by adding T mod Ns
+// (no division per butterfly).  (Padding the row as the power-of-two kernels do made these
+// passes slower: their strides are multiples of 3 and 5.)
 template <int R, bool INV>
 __device__ __forceinline__ void mixed_pass(float2* lds, int N, int Ns) {
   constexpr int MB = (kMixedMaxPerThread + R - 1) / R;  // butterflies per thread, at most
@@ -104,13 +111,19 @@ __device__ __forceinline__ void mixed_pass(float2* lds, int N, int Ns) {
     }
   }
   __syncthreads();
+  const float inv_den = 1.0f / (float)(Ns * R);
+  const int step = T % Ns;
+  int k = t % Ns;  // k of butterfly t + s*T, advanced by step per s
 #pragma unroll
   for (int s = 0; s < MB; ++s) {
     const int j = t + s * T;
+    if (s > 0) {
+      k += step;
+      if (k >= Ns) k -= Ns;
+    }
     if (j < B) {
-      const int k = j % Ns;
       if (Ns > 1) {
-        const float2 w1 = unit_root_dev<INV>(k, Ns * R);
+        const float2 w1 = unit_root_dev<INV>(k, inv_den);
         float2 w = w1;
 #pragma unroll
         for (int r = 1; r < R; ++r) {
@@ -156,7 +169,7 @@ __global__ void __launch_bounds__(1024) mixed_rows_kernel(Elem* buf, MixedPlan p
   } else {
     // pre-pass: Z~_m = (s + i conj(W_n^m) d) / n, Z~_{N-m} = conj(s - i conj(W_n^m) d) / n with
     // s = Y_m + conj(Y_{N-m}), d = Y_m - conj(Y_{N-m}); slot 0 holds (Y_0, Y_{n/2})
-    const float sc = 1.0f / (2.0f * N);
+    const float sc = 1.0f / (2.0f * N), inv_n = 1.0f / (float)(2 * N);
     for (int m = t; 2 * m <= N; m += T) {
       const float2 ya = spec.load(m);
       if (m == 0) {
@@ -165,7 +178,7 @@ __global__ void __launch_bounds__(1024) mixed_rows_kernel(Elem* buf, MixedPlan p
       }
       const float2 yb = c_conj(spec.load(N - m));
       const float2 s = c_add(ya, yb), d = c_sub(ya, yb);
-      const float2 w = unit_root_dev<true>(m, 2 * N);         // conj(W_n^m)
+      const float2 w = unit_root_dev<true>(m, inv_n);         // conj(W_n^m)
       const float2 q = c_mul<false>(d, make_float2(-sc * w.y, sc * w.x));  // i conj(W_n^m) d / n
       mixed_lds[m] = make_float2(fmaf(s.x, sc, q.x), fmaf(s.y, sc, q.y));
       if (2 * m != N) mixed_lds[N - m] = make_float2(fmaf(s.x, sc, -q.x), -fmaf(s.y, sc, -q.y));
@@ -176,6 +189,7 @@ __global__ void __launch_bounds__(1024) mixed_rows_kernel(Elem* buf, MixedPlan p
   if constexpr (!INV) {
     // post-pass: Y_k = s/2 + (-i W_n^k / 2) d, Y_{N-k} = conj(s/2 - (-i W_n^k / 2) d) with
     // s = Z_k + conj(Z_{N-k}), d = Z_k - conj(Z_{N-k}); slot 0 = (Y_0, Y_{n/2})
+    const float inv_n = 1.0f / (float)(2 * N);
     for (int k = t; 2 * k <= N; k += T) {
       const float2 a = mixed_lds[k];
       if (k == 0) {
@@ -184,7 +198,7 @@ __global__ void __launch_bounds__(1024) mixed_rows_kernel(Elem* buf, MixedPlan p
       }
       const float2 b = c_conj(mixed_lds[N - k]);
       const float2 s = c_add(a, b), d = c_sub(a, b);
-      const float2 w = unit_root_dev<false>(k, 2 * N);  // W_n^k
+      const float2 w = unit_root_dev<false>(k, inv_n);  // W_n^k
       const float2 q = c_mul<false>(d, make_float2(0.5f * w.y, -0.5f * w.x));  // -i W_n^k d / 2
       spec.store(k, make_float2(fmaf(s.x, 0.5f, q.x), fmaf(s.y, 0.5f, q.y)));
       if (2 * k != N) spec.store(N - k, make_float2(fmaf(s.x, 0.5f, -q.x), -fmaf(s.y, 0.5f, -q.y)));
