@@ -339,7 +339,9 @@ def config_table(dev, stream, reps: int = 10):
 def encoder_step(dev, stream, queue_behind_spin, reps: int = 5):
     """The encoder-style configuration as one step: forward and backward of the 768-wide
     p = 256 bf16 layer (4096 tokens) for 24 instances, the query and value projections of
-    12 layers, each with its own x, y, gy, dx, spectra and dc (every instance's forward,
+    12 layers, each with its own x, y, gy, dx, spectra and dc.  Timed two ways: the 24
+    instances as one batch (`bca_forward_batched`, then `bca_backward_batched`: the layers
+    side by side in the same launches), and one call per instance (every instance's forward,
     then every instance's backward).  Algorithmic bytes per instance: forward x, y and the
     spectra; backward x, gy, dx, the spectra and dc."""
     import torch
@@ -355,26 +357,38 @@ def encoder_step(dev, stream, queue_behind_spin, reps: int = 5):
                   dx=torch.empty(T, d, device=dev, dtype=torch.bfloat16),
                   dc=torch.empty(q, kb, p, device=dev)) for _ in range(n_inst)]
 
-    def step():
+    lists = {k: [st[k] for st in insts] for k in ("x", "c", "g", "y", "dx", "dc")}
+
+    def batched_step():
+        api.bca_forward_batched(lists["x"], lists["c"], lists["y"])
+        api.bca_backward_batched(lists["x"], lists["c"], lists["g"], lists["dx"], lists["dc"])
+
+    def per_call_step():
         for st in insts:
             api.bca_forward(st["x"], st["c"], st["y"])
         for st in insts:
             api.bca_backward(st["x"], st["c"], st["g"], st["dx"], st["dc"])
 
-    step()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    queue_behind_spin()
-    e0.record(stream)
-    for _ in range(reps):
+    def timed_step(step):
         step()
-    e1.record(stream)
-    torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) * 1e3 / reps
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        queue_behind_spin()
+        e0.record(stream)
+        for _ in range(reps):
+            step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    us = timed_step(batched_step)
+    us_calls = timed_step(per_call_step)
     nbytes = n_inst * ((2 * T * d * 2 + q * kb * p * 2) + (3 * T * d * 2 + q * kb * p * 2 + q * kb * p * 4))
-    del insts
+    del insts, lists
     torch.cuda.empty_cache()
     return {"instances": n_inst, "step_us": round(us, 2), "GB_s": round(nbytes / us / 1e3, 1),
-            "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "bytes_per_step": nbytes}
+            "frac": round(nbytes / us / 1e3 / HBM_PEAK_GBS, 4), "bytes_per_step": nbytes,
+            "one_call_per_instance": {"step_us": round(us_calls, 2), "GB_s": round(nbytes / us_calls / 1e3, 1),
+                                      "frac": round(nbytes / us_calls / 1e3 / HBM_PEAK_GBS, 4)}}
 
 
 def copy_rate(dev, stream, reps: int = 5):

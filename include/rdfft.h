@@ -176,6 +176,32 @@ RDFFT_API int bca_forward(const void *x, const void *c_spectra, void *y, bca_gra
 RDFFT_API int bca_backward(const void *x, const void *c_spectra, void *gy, bca_grads_t *grads, int64_t d_in,
                  int64_t d_out, int64_t p, int64_t tokens, rdfft_dtype_t dtype, rdfft_stream_t stream);
 
+/*
+ * bca_forward_batched / bca_backward_batched -- `count` independent layers of one shape
+ * (the same d_in, d_out, p, tokens and dtype, each with its own tensors), such as the query
+ * and value adapters of every layer of an encoder (Sec. 5.1.2), in one call.  Square layers
+ * of 128 <= p <= 512 with q = kb <= 4 (the ones whose transforms fit a wavefront) run the
+ * layers side by side in the same launches, which fills the chip where one layer alone
+ * cannot; the backward does so when every dx is apart from its gy.  Other batches run
+ * their layers one after another.  Results equal those of bca_forward / bca_backward on
+ * each layer (dc up to the order of its float32 sums).
+ *   count      0 <= count <= 1024 (0: no-op); else RDFFT_EINVAL.
+ *   x, c_spectra, y / gy
+ *              host arrays of `count` device pointers, entry b as the argument of the
+ *              single-layer call for layer b.
+ *   grads      host array of `count` bca_grads_t (backward only).
+ * Within a layer the aliasing rules of the single-layer calls hold.  Across layers, buffers
+ * that are only read may be shared (one x for several layers), but nothing a layer writes
+ * (y; gy, dx, dc) may overlap any buffer of another layer -> RDFFT_EINVAL.  All layers are
+ * checked before anything is enqueued.
+ */
+RDFFT_API int bca_forward_batched(int count, const void *const *x, const void *const *c_spectra, void *const *y,
+                                  int64_t d_in, int64_t d_out, int64_t p, int64_t tokens, rdfft_dtype_t dtype,
+                                  rdfft_stream_t stream);
+RDFFT_API int bca_backward_batched(int count, const void *const *x, const void *const *c_spectra, void *const *gy,
+                                   const bca_grads_t *grads, int64_t d_in, int64_t d_out, int64_t p, int64_t tokens,
+                                   rdfft_dtype_t dtype, rdfft_stream_t stream);
+
 /* Uploads the twiddle table to the current device (synchronously) if not done yet.
  * Optional: every entry point does it on first use.  Returns RDFFT_OK or RDFFT_EDEVICE. */
 RDFFT_API int rdfft_init(void);

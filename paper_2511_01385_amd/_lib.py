@@ -31,6 +31,8 @@ EXPORTS = (
     "rdfft_inverse_halfcomplex",
     "bca_forward",
     "bca_backward",
+    "bca_forward_batched",
+    "bca_backward_batched",
     "rdfft_init",
     "rdfft_table_bytes",
     "rdfft_status_string",
@@ -63,6 +65,11 @@ def load() -> ctypes.CDLL:
         f = getattr(lib, name)
         f.argtypes = [vp, vp, vp, ctypes.POINTER(BcaGrads), i64, i64, i64, i64, i32, vp]
         f.restype = i32
+    pp = ctypes.POINTER(ctypes.c_void_p)
+    lib.bca_forward_batched.argtypes = [i32, pp, pp, pp, i64, i64, i64, i64, i32, vp]
+    lib.bca_forward_batched.restype = i32
+    lib.bca_backward_batched.argtypes = [i32, pp, pp, pp, ctypes.POINTER(BcaGrads), i64, i64, i64, i64, i32, vp]
+    lib.bca_backward_batched.restype = i32
     lib.rdfft_init.argtypes = []
     lib.rdfft_init.restype = i32
     lib.rdfft_table_bytes.argtypes = []

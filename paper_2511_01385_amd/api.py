@@ -138,8 +138,8 @@ def bca_forward(x: torch.Tensor, c_spectra: torch.Tensor, y: torch.Tensor) -> to
 def bca_backward(x: torch.Tensor, c_spectra: torch.Tensor, gy: torch.Tensor, dx: torch.Tensor, dc: torch.Tensor):
     """Writes dL/dx into ``dx`` and dL/dc (float32, time domain, shape (q, kb, p)) into ``dc``.
 
-    ``gy`` is left unspecified; ``dx`` may be ``gy`` itself when d_in == d_out and p <= 8192
-    (longer blocks stage the input spectra in ``dx``).
+    ``gy`` is left unspecified; ``dx`` may be ``gy`` itself when d_in == d_out (for blocks
+    beyond 8192, with at most 8 blocks per row).
     """
     q, kb, p, tokens = _layer_shapes(x, c_spectra, gy, "gy")
     if tuple(dx.shape) != tuple(x.shape) or dx.dtype != x.dtype or dx.device != x.device:
@@ -155,6 +155,53 @@ def bca_backward(x: torch.Tensor, c_spectra: torch.Tensor, gy: torch.Tensor, dx:
     )
     _check(st, "bca_backward")
     return dx, dc
+
+
+def _pointer_array(ts, name):
+    return (ctypes.c_void_p * len(ts))(*[_dev(t, f"{name}[{i}]") for i, t in enumerate(ts)])
+
+
+def _batch_shapes(xs, cs, outs, out_name):
+    if not (len(xs) == len(cs) == len(outs)):
+        raise ValueError("one x, c_spectra and output per layer")
+    shapes = {_layer_shapes(x, c, o, out_name) for x, c, o in zip(xs, cs, outs)}
+    if len(shapes) != 1 or len({x.dtype for x in xs}) != 1 or len({x.device for x in xs}) != 1:
+        raise ValueError("the layers of a batch share one shape, storage type and device")
+    return shapes.pop()
+
+
+def bca_forward_batched(xs, c_spectras, ys):
+    """``bca_forward`` for several independent layers of one shape (lists of tensors), in one call."""
+    if len(xs) == 0:
+        return ys
+    q, kb, p, tokens = _batch_shapes(xs, c_spectras, ys, "y")
+    st = _lib.load().bca_forward_batched(
+        len(xs), _pointer_array(xs, "x"), _pointer_array(c_spectras, "c_spectra"), _pointer_array(ys, "y"),
+        kb * p, q * p, p, tokens, _code(xs[0]), _stream(xs[0]),
+    )
+    _check(st, "bca_forward_batched")
+    return ys
+
+
+def bca_backward_batched(xs, c_spectras, gys, dxs, dcs):
+    """``bca_backward`` for several independent layers of one shape (lists of tensors), in one call."""
+    if len(xs) == 0:
+        return dxs, dcs
+    q, kb, p, tokens = _batch_shapes(xs, c_spectras, gys, "gy")
+    if not (len(dxs) == len(dcs) == len(xs)):
+        raise ValueError("one dx and dc per layer")
+    for x, dx, dc in zip(xs, dxs, dcs):
+        if tuple(dx.shape) != tuple(x.shape) or dx.dtype != x.dtype or dx.device != x.device:
+            raise ValueError(f"dx must match x: {tuple(x.shape)} {x.dtype} on {x.device}")
+        if tuple(dc.shape) != (q, kb, p) or dc.device != x.device or dc.dtype != torch.float32:
+            raise ValueError(f"dc must be float32 of shape ({q}, {kb}, {p}) on {x.device}")
+    grads = (_lib.BcaGrads * len(xs))(*[_lib.BcaGrads(_dev(dx, "dx"), _dev(dc, "dc")) for dx, dc in zip(dxs, dcs)])
+    st = _lib.load().bca_backward_batched(
+        len(xs), _pointer_array(xs, "x"), _pointer_array(c_spectras, "c_spectra"), _pointer_array(gys, "gy"), grads,
+        kb * p, q * p, p, tokens, _code(xs[0]), _stream(xs[0]),
+    )
+    _check(st, "bca_backward_batched")
+    return dxs, dcs
 
 
 def rdfft_init() -> None:

@@ -33,11 +33,14 @@ constexpr int finish_wg() {
   return RowPlan<LOGN>::TPR > 64 ? RowPlan<LOGN>::TPR : (N < 64 ? 64 : (N > 1024 ? 1024 : N));
 }
 
-template <int LOGN>
-__global__ void __launch_bounds__(finish_wg<LOGN>()) bca_dc_finish_kernel(const float2* __restrict__ stage,
-                                                                          float* __restrict__ dc, int rows_ij,
-                                                                          int chunk, int groups, int64_t tile_f2,
+// Layer b of a batch (grid row blockIdx.y when MAXB > 1) reads p.stage[b] and adds into p.dc[b].
+template <int LOGN, int MAXB>
+__global__ void __launch_bounds__(finish_wg<LOGN>()) bca_dc_finish_kernel(FinishPtrs<MAXB> fp, int rows_ij, int chunk,
+                                                                          int groups, int64_t tile_f2,
                                                                           const float2* __restrict__ tw) {
+  const int bi = MAXB == 1 ? 0 : (int)blockIdx.y;
+  const float2* __restrict__ stage = fp.stage[bi];
+  float* __restrict__ dc = fp.dc[bi];
   using P = RowPlan<LOGN>;
   constexpr int N = P::N, TPR = P::TPR, WG = finish_wg<LOGN>();
   constexpr int REG = P::LDS_F2 > lds_padded_size(N) ? P::LDS_F2 : lds_padded_size(N);
@@ -69,27 +72,35 @@ __global__ void __launch_bounds__(finish_wg<LOGN>()) bca_dc_finish_kernel(const 
     row_inverse<LOGN, true>((int)threadIdx.x, true, LdsSpectrum{reg}, AtomicAddF32{dc + (int64_t)ij * 2 * N}, reg, tw);
 }
 
-template <int LOGN>
-static hipError_t dc_finish_launch(const float2* stage, float* dc, int rows_ij, int chunk, int groups, int64_t tile_f2,
-                                   const float2* tw, hipStream_t stream) {
+template <int LOGN, int MAXB>
+static hipError_t dc_finish_launch(const FinishPtrs<MAXB>& fp, int count, int rows_ij, int chunk, int groups,
+                                   int64_t tile_f2, const float2* tw, hipStream_t stream) {
   const int units = rows_ij * ((groups + kReduceGroup - 1) / kReduceGroup);
-  hipLaunchKernelGGL(bca_dc_finish_kernel<LOGN>, dim3((unsigned)units), dim3(finish_wg<LOGN>()), 0, stream, stage, dc,
-                     rows_ij, chunk, groups, tile_f2, tw);
+  hipLaunchKernelGGL((bca_dc_finish_kernel<LOGN, MAXB>), dim3((unsigned)units, (unsigned)count),
+                     dim3(finish_wg<LOGN>()), 0, stream, fp, rows_ij, chunk, groups, tile_f2, tw);
   return hipGetLastError();
 }
 
-template <int... L>
-static std::array<hipError_t (*)(const float2*, float*, int, int, int, int64_t, const float2*, hipStream_t),
+template <int MAXB, int... L>
+static std::array<hipError_t (*)(const FinishPtrs<MAXB>&, int, int, int, int, int64_t, const float2*, hipStream_t),
                   sizeof...(L)>
 dc_finish_table(std::integer_sequence<int, L...>) {
-  return {&dc_finish_launch<L>...};
+  return {&dc_finish_launch<L, MAXB>...};
 }
 
 hipError_t launch_dc_finish(const float2* stage, float* dc, int rows_ij, int logn, int chunk, int groups,
                             int64_t tile_f2, const float2* tw, hipStream_t stream) {
-  static const auto tab = dc_finish_table(std::make_integer_sequence<int, kBcaMaxLogN + 1>{});
+  static const auto tab = dc_finish_table<1>(std::make_integer_sequence<int, kBcaMaxLogN + 1>{});
   if (logn < 0 || logn > kBcaMaxLogN) return hipErrorInvalidValue;
-  return tab[logn](stage, dc, rows_ij, chunk, groups, tile_f2, tw, stream);
+  const FinishPtrs<1> fp{{stage}, {dc}};
+  return tab[logn](fp, 1, rows_ij, chunk, groups, tile_f2, tw, stream);
+}
+
+hipError_t launch_dc_finish_batched(const FinishPtrs<kMaxBatch>& fp, int count, int rows_ij, int logn, int chunk,
+                                    int groups, int64_t tile_f2, const float2* tw, hipStream_t stream) {
+  static const auto tab = dc_finish_table<kMaxBatch>(std::make_integer_sequence<int, kBcaMaxLogN + 1>{});
+  if (logn < 0 || logn > kBcaMaxLogN || count < 1 || count > kMaxBatch) return hipErrorInvalidValue;
+  return tab[logn](fp, count, rows_ij, chunk, groups, tile_f2, tw, stream);
 }
 
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
@@ -132,6 +143,30 @@ hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t st
     if (fn != nullptr) return fn(a, tw, stream, num_cu);
   }
   return t.fwd[a.logp - 1](a, tw, stream);
+}
+
+bool bca_batch_fused(int logp, int q, int kb, int storage, bool backward) {
+  if (storage < 0 || storage >= kStorages || q != kb || q < 1 || q > kSqMaxBlocks) return false;
+  const int logn = logp - 1;
+  if (logn < 0 || logn > kBcaMaxLogN) return false;
+  const BcaStoreTables& t = store_tables(storage);
+  return (backward ? t.wave_bwd_batched : t.wave_fwd_batched)[q - 1][logn] != nullptr;
+}
+
+hipError_t launch_bca_forward_batched(const BcaArgs& a, const BcaBatch& b, const float2* tw, hipStream_t stream,
+                                      int num_cu) {
+  if (!bca_batch_fused(a.logp, a.q, a.kb, a.storage, false) || b.count < 1 || b.count > kMaxBatch)
+    return hipErrorInvalidValue;
+  return store_tables(a.storage).wave_fwd_batched[a.q - 1][a.logp - 1](a, b, tw, stream, num_cu);
+}
+
+// Every layer's dx apart from its gy (the caller checks): the staged two-stage dC sum, which
+// also zeroes dc and leaves it in the time domain.
+hipError_t launch_bca_backward_batched(const BcaArgs& a, const BcaBatch& b, const float2* tw, hipStream_t stream,
+                                       int num_cu) {
+  if (!bca_batch_fused(a.logp, a.q, a.kb, a.storage, true) || b.count < 1 || b.count > kMaxBatch || a.tokens < 1)
+    return hipErrorInvalidValue;
+  return store_tables(a.storage).wave_bwd_batched[a.q - 1][a.logp - 1](a, b, tw, stream, num_cu);
 }
 
 hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {

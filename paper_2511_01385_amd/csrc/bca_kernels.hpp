@@ -830,15 +830,29 @@ constexpr int wave_tokens() {
   return G % QB == 0 ? G / QB : (G >= 2 * QB ? G / QB : 1);
 }
 
+// The tensors of the layers a wave-kernel launch serves: layer b (grid row blockIdx.y when
+// MAXB > 1) reads x[b], c[b] and writes y[b] (forward), or reads x[b], c[b], y[b] = gy and
+// writes dx[b], dc[b] (backward).
+template <class St, int MAXB>
+struct WavePtrs {
+  const ElemOf<St>* x[MAXB];
+  const ElemOf<St>* c[MAXB];
+  ElemOf<St>* y[MAXB];
+  ElemOf<St>* dx[MAXB];
+  float* dc[MAXB];
+};
+
 // Forward: per group, X_j = rdFFT(x_j) into the wave's LDS regions, Y_i = sum_j C_ij X_j
 // per bin written over X_i (a lane reads every X_j[k] of its bin before it writes), then
 // y_i = irdFFT(Y_i).  y may be x: a wave reads its group's x rows before it writes the
 // group's y rows, and no other wave touches them.
-template <int LOGN, class St, int QB, int TW, int NW = kWaveFwdNW>
+template <int LOGN, class St, int QB, int TW, int MAXB, int NW = kWaveFwdNW>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWaveMinWaves)))
-bca_forward_wave_kernel(const ElemOf<St>* x, const ElemOf<St>* __restrict__ c,
-                                                                   ElemOf<St>* y, int64_t tokens, int64_t ngroups,
-                                                                   const float2* __restrict__ tw) {
+bca_forward_wave_kernel(WavePtrs<St, MAXB> ptrs, int64_t tokens, int64_t ngroups, const float2* __restrict__ tw) {
+  const int bi = MAXB == 1 ? 0 : (int)blockIdx.y;
+  const ElemOf<St>* x = ptrs.x[bi];
+  const ElemOf<St>* __restrict__ c = ptrs.c[bi];
+  ElemOf<St>* y = ptrs.y[bi];
   using W = BcaWave<LOGN, QB>;
   using In = typename St::In;
   using Out = typename St::Out;
@@ -916,14 +930,17 @@ bca_forward_wave_kernel(const ElemOf<St>* x, const ElemOf<St>* __restrict__ c,
 // workgroup's four waves add their dC in LDS, and the sum goes to dc by float32 atomics
 // (stage == nullptr; dc zeroed beforehand) or is written to `stage` at
 // blockIdx.x * stage_f2 for bca_dc_finish_kernel (then this kernel zeroes dc).
-template <int LOGN, class St, int QB, int TW, int NW = kWaveBwdNW>
+template <int LOGN, class St, int QB, int TW, int MAXB, int NW = kWaveBwdNW>
 __global__ void __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(kWaveBwdMinWaves)))
-bca_backward_wave_kernel(const ElemOf<St>* __restrict__ x,
-                                                                    const ElemOf<St>* __restrict__ c,
-                                                                    const ElemOf<St>* gy, ElemOf<St>* dx,
-                                                                    float* __restrict__ dc, int64_t tokens,
-                                                                    int64_t ngroups, float2* stage, int64_t stage_f2,
-                                                                    const float2* __restrict__ tw) {
+bca_backward_wave_kernel(WavePtrs<St, MAXB> ptrs, int64_t tokens, int64_t ngroups, int staged, int64_t stage_f2,
+                         const float2* __restrict__ tw) {
+  const int bi = MAXB == 1 ? 0 : (int)blockIdx.y;
+  const ElemOf<St>* __restrict__ x = ptrs.x[bi];
+  const ElemOf<St>* __restrict__ c = ptrs.c[bi];
+  const ElemOf<St>* gy = ptrs.y[bi];
+  ElemOf<St>* dx = ptrs.dx[bi];
+  float* __restrict__ dc = ptrs.dc[bi];
+  float2* const stage = staged ? reinterpret_cast<float2*>(ptrs.y[bi]) : nullptr;
   using W = BcaWave<LOGN, QB>;
   using In = typename St::In;
   using Out = typename St::Out;
@@ -1053,54 +1070,120 @@ constexpr size_t wave_lds_bytes(bool backward) {
   return spectra > part ? spectra : part;
 }
 
-template <int LOGN, class St, int QB>
-static hipError_t fwd_wave_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+// Wave-kernel launches for `count` layers of one shape (count <= MAXB).  Layers share the
+// chip: each gets about 1/count of the workgroups one layer alone would get.
+template <int LOGN, class St, int QB, int MAXB>
+static hipError_t fwd_wave_launch(const WavePtrs<St, MAXB>& ptrs, int count, int64_t tokens, const float2* tw,
+                                  hipStream_t stream, int num_cu) {
   constexpr int TW = wave_tokens<LOGN, QB>(), NW = kWaveFwdNW;
   constexpr size_t lds = wave_lds_bytes<LOGN, QB>(false);
   static_assert(lds <= (size_t)kLdsLimit, "wave groups too large for LDS");
-  static const hipError_t attr = set_lds_limit(bca_forward_wave_kernel<LOGN, St, QB, TW>);
+  static const hipError_t attr = set_lds_limit(bca_forward_wave_kernel<LOGN, St, QB, TW, MAXB>);
   if (attr != hipSuccess) return attr;
-  const int64_t groups = (a.tokens + TW - 1) / TW;
+  const int64_t groups = (tokens + TW - 1) / TW;
   // every wave takes groups until none are left; enough workgroups for a full chip
   const int per_cu = std::max(1, std::min<int>(kLdsLimit / (int)lds, 2048 / (64 * NW)));
-  const int64_t grid = std::min<int64_t>((groups + NW - 1) / NW, (int64_t)num_cu * per_cu);
-  hipLaunchKernelGGL((bca_forward_wave_kernel<LOGN, St, QB, TW>), dim3((unsigned)grid), dim3(64 * NW), lds, stream,
-                     static_cast<const ElemOf<St>*>(a.x), static_cast<const ElemOf<St>*>(a.c),
-                     static_cast<ElemOf<St>*>(a.y), a.tokens, groups, tw);
+  const int64_t slots = ((int64_t)num_cu * per_cu + count - 1) / count;
+  const int64_t grid = std::max<int64_t>(1, std::min<int64_t>((groups + NW - 1) / NW, slots));
+  hipLaunchKernelGGL((bca_forward_wave_kernel<LOGN, St, QB, TW, MAXB>), dim3((unsigned)grid, (unsigned)count),
+                     dim3(64 * NW), lds, stream, ptrs, tokens, groups, tw);
   return hipGetLastError();
 }
 
 template <int LOGN, class St, int QB>
-static hipError_t bwd_wave_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+static hipError_t fwd_wave_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  const WavePtrs<St, 1> p{{static_cast<const ElemOf<St>*>(a.x)}, {static_cast<const ElemOf<St>*>(a.c)},
+                          {static_cast<ElemOf<St>*>(a.y)}, {nullptr}, {nullptr}};
+  return fwd_wave_launch<LOGN, St, QB, 1>(p, 1, a.tokens, tw, stream, num_cu);
+}
+
+// The two-stage dC sum of `count` layers: layer b's partials in its own gy rows, its sum in
+// its own dc (bca_kernels.hip)
+template <int MAXB>
+struct FinishPtrs {
+  const float2* stage[MAXB];
+  float* dc[MAXB];
+};
+hipError_t launch_dc_finish_batched(const FinishPtrs<kMaxBatch>& p, int count, int rows_ij, int logn, int chunk,
+                                    int groups, int64_t tile_f2, const float2* tw, hipStream_t stream);
+
+template <int LOGN, class St, int QB, int MAXB>
+static hipError_t bwd_wave_launch(const WavePtrs<St, MAXB>& ptrs, int count, bool apart, int64_t tokens,
+                                  const float2* tw, hipStream_t stream, int num_cu) {
   using W = BcaWave<LOGN, QB>;
   constexpr int TW = wave_tokens<LOGN, QB>(), NW = kWaveBwdNW;
   constexpr size_t lds = wave_lds_bytes<LOGN, QB>(true);
   static_assert(lds <= (size_t)kLdsLimit, "wave groups too large for LDS");
   constexpr int QKN = QB * QB * W::N;
-  static const hipError_t attr = set_lds_limit(bca_backward_wave_kernel<LOGN, St, QB, TW>);
+  static const hipError_t attr = set_lds_limit(bca_backward_wave_kernel<LOGN, St, QB, TW, MAXB>);
   if (attr != hipSuccess) return attr;
-  const int64_t groups = (a.tokens + TW - 1) / TW;
-  // one workgroup per CU: fewer workgroups, fewer dC partial sums to add
-  const int64_t grid = std::min<int64_t>((groups + NW - 1) / NW, (int64_t)num_cu);
-  // Two-stage dC sum when dx has its own buffer: workgroup b's first groups are the
+  const int64_t groups = (tokens + TW - 1) / TW;
+  // one workgroup per CU in all: fewer workgroups, fewer dC partial sums to add
+  const int64_t grid = std::max<int64_t>(1, std::min<int64_t>((groups + NW - 1) / NW, num_cu / count));
+  // Two-stage dC sum when dx has its own buffer (apart): workgroup b's first groups are the
   // tokens [b*NW*TW, (b+1)*NW*TW), whose gy rows only it reads; once all its waves are
   // done it writes its partial sums there (QKN float2 must fit those rows, all of them
   // valid tokens)
   const int64_t region_f2 = (int64_t)NW * TW * QB * W::N * (int64_t)sizeof(ElemOf<St>) / (int64_t)sizeof(float2);
-  const bool staged = a.dx != a.y && region_f2 >= QKN && grid * NW * TW <= a.tokens;
-  float2* const stage = staged ? static_cast<float2*>(a.y) : nullptr;
+  const bool staged = apart && region_f2 >= QKN && grid * NW * TW <= tokens;
+  if (!staged && count > 1) {
+    // too few tokens to stage a batch's partial sums: the layers one by one
+    for (int b = 0; b < count; ++b) {
+      const WavePtrs<St, 1> p1{{ptrs.x[b]}, {ptrs.c[b]}, {ptrs.y[b]}, {ptrs.dx[b]}, {ptrs.dc[b]}};
+      const hipError_t e1 = bwd_wave_launch<LOGN, St, QB, 1>(p1, 1, apart, tokens, tw, stream, num_cu);
+      if (e1 != hipSuccess) return e1;
+    }
+    return hipSuccess;
+  }
   if (!staged) {
-    const hipError_t ez = launch_fill_zero(a.dc, 2 * (int64_t)QKN, stream);
+    const hipError_t ez = launch_fill_zero(ptrs.dc[0], 2 * (int64_t)QKN, stream);
     if (ez != hipSuccess) return ez;
   }
-  hipLaunchKernelGGL((bca_backward_wave_kernel<LOGN, St, QB, TW>), dim3((unsigned)grid), dim3(64 * NW), lds, stream,
-                     static_cast<const ElemOf<St>*>(a.x), static_cast<const ElemOf<St>*>(a.c),
-                     static_cast<const ElemOf<St>*>(a.y), static_cast<ElemOf<St>*>(a.dx), a.dc, a.tokens, groups, stage,
-                     region_f2, tw);
+  hipLaunchKernelGGL((bca_backward_wave_kernel<LOGN, St, QB, TW, MAXB>), dim3((unsigned)grid, (unsigned)count),
+                     dim3(64 * NW), lds, stream, ptrs, tokens, groups, staged ? 1 : 0, region_f2, tw);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  if (staged) return launch_dc_finish(stage, a.dc, QB * QB, LOGN, QKN, (int)grid, region_f2, tw, stream);
-  return launch_rdfft_rows(a.dc, (int64_t)QB * QB, LOGN, kStorageF32, true, tw, stream, num_cu);
+  if (staged) {
+    FinishPtrs<kMaxBatch> f{};
+    for (int b = 0; b < count; ++b) {
+      f.stage[b] = reinterpret_cast<const float2*>(ptrs.y[b]);
+      f.dc[b] = ptrs.dc[b];
+    }
+    return launch_dc_finish_batched(f, count, QB * QB, LOGN, QKN, (int)grid, region_f2, tw, stream);
+  }
+  return launch_rdfft_rows(ptrs.dc[0], (int64_t)QB * QB, LOGN, kStorageF32, true, tw, stream, num_cu);
+}
+
+template <int LOGN, class St, int QB>
+static hipError_t bwd_wave_impl(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu) {
+  const WavePtrs<St, 1> p{{static_cast<const ElemOf<St>*>(a.x)}, {static_cast<const ElemOf<St>*>(a.c)},
+                          {static_cast<ElemOf<St>*>(a.y)}, {static_cast<ElemOf<St>*>(a.dx)}, {a.dc}};
+  return bwd_wave_launch<LOGN, St, QB, 1>(p, 1, a.dx != a.y, a.tokens, tw, stream, num_cu);
+}
+
+// Batches: kMaxBatch-wide pointer lists, count layers in grid rows
+template <int LOGN, class St>
+static WavePtrs<St, kMaxBatch> batch_ptrs(const BcaBatch& b) {
+  WavePtrs<St, kMaxBatch> p{};
+  for (int i = 0; i < b.count; ++i) {
+    p.x[i] = static_cast<const ElemOf<St>*>(b.x[i]);
+    p.c[i] = static_cast<const ElemOf<St>*>(b.c[i]);
+    p.y[i] = static_cast<ElemOf<St>*>(b.y[i]);
+    p.dx[i] = static_cast<ElemOf<St>*>(b.dx[i]);
+    p.dc[i] = b.dc[i];
+  }
+  return p;
+}
+template <int LOGN, class St, int QB>
+static hipError_t fwd_wave_batched(const BcaArgs& a, const BcaBatch& b, const float2* tw, hipStream_t stream,
+                                   int num_cu) {
+  return fwd_wave_launch<LOGN, St, QB, kMaxBatch>(batch_ptrs<LOGN, St>(b), b.count, a.tokens, tw, stream, num_cu);
+}
+template <int LOGN, class St, int QB>
+static hipError_t bwd_wave_batched(const BcaArgs& a, const BcaBatch& b, const float2* tw, hipStream_t stream,
+                                   int num_cu) {
+  return bwd_wave_launch<LOGN, St, QB, kMaxBatch>(batch_ptrs<LOGN, St>(b), b.count, true, a.tokens, tw, stream,
+                                                  num_cu);
 }
 
 using BcaFn = hipError_t (*)(const BcaArgs&, const float2*, hipStream_t);
@@ -1150,6 +1233,9 @@ static SqTable sq_bwd_tables() {
 
 // The launchers of one storage type, indexed by log2(p/2) (and q - 1 for the square-layer
 // kernels; nullptr where those kernels do not fit).
+using BcaBatchFn = hipError_t (*)(const BcaArgs&, const BcaBatch&, const float2*, hipStream_t, int);
+using BatchTable = std::array<std::array<BcaBatchFn, kBcaMaxLogN + 1>, kSqMaxBlocks>;
+
 struct BcaStoreTables {
   std::array<BcaFn, kBcaMaxLogN + 1> fwd;
   std::array<BcaBwdFn, kBcaMaxLogN + 1> bwd;
@@ -1157,6 +1243,8 @@ struct BcaStoreTables {
   SqTable sq_bwd;
   SqTable wave_fwd;
   SqTable wave_bwd;
+  BatchTable wave_fwd_batched;
+  BatchTable wave_bwd_batched;
 };
 
 template <int LOGN, class St, int QB>
@@ -1179,10 +1267,30 @@ static SqTable wave_tables(bool backward) {
           wave_row<St, 4>(backward, SeqP{})};
 }
 
+template <int LOGN, class St, int QB>
+static constexpr BcaBatchFn batch_entry(bool backward) {
+  if constexpr (wave_fits<LOGN, QB>(true)) {
+    return backward ? &bwd_wave_batched<LOGN, St, QB> : &fwd_wave_batched<LOGN, St, QB>;
+  } else if constexpr (wave_fits<LOGN, QB>(false)) {
+    return backward ? nullptr : &fwd_wave_batched<LOGN, St, QB>;
+  } else {
+    return nullptr;
+  }
+}
+template <class St, int QB, int... L>
+static std::array<BcaBatchFn, sizeof...(L)> batch_row(bool backward, std::integer_sequence<int, L...>) {
+  return {batch_entry<L, St, QB>(backward)...};
+}
+template <class St>
+static BatchTable batch_tables(bool backward) {
+  return {batch_row<St, 1>(backward, SeqP{}), batch_row<St, 2>(backward, SeqP{}), batch_row<St, 3>(backward, SeqP{}),
+          batch_row<St, 4>(backward, SeqP{})};
+}
+
 template <class St>
 BcaStoreTables make_store_tables() {
-  return {fwd_row<St>(SeqP{}),      bwd_row<St>(SeqP{}),     sq_fwd_tables<St>(),
-          sq_bwd_tables<St>(),      wave_tables<St>(false), wave_tables<St>(true)};
+  return {fwd_row<St>(SeqP{}),     bwd_row<St>(SeqP{}),     sq_fwd_tables<St>(),    sq_bwd_tables<St>(),
+          wave_tables<St>(false), wave_tables<St>(true),  batch_tables<St>(false), batch_tables<St>(true)};
 }
 
 BcaStoreTables bca_tables_f32();

@@ -153,6 +153,58 @@ int check_bca(const void* x, const void* c, const void* y, int64_t d_in, int64_t
   return RDFFT_OK;
 }
 
+// bca_forward's checks beyond check_bca (tokens > 0): y may be x itself (an in-place layer)
+// only when the shapes agree
+int check_forward_alias(const void* x, const void* y, int64_t d_in, int64_t d_out, int64_t p, const BcaShape& sh) {
+  if (y == x) {
+    if (d_in != d_out) return RDFFT_EINVAL;
+    if (p > 8192 && sh.q > rdfft::kMpMaxInPlaceBlocks) return RDFFT_EUNSUPPORTED;
+  } else if (overlaps(x, sh.x_bytes, y, sh.y_bytes)) {
+    return RDFFT_EINVAL;
+  }
+  return RDFFT_OK;
+}
+
+// bca_backward's checks beyond check_bca
+int check_backward_grads(const void* x, const void* c_spectra, const void* gy, const void* dx, const float* dc,
+                         int64_t d_in, int64_t d_out, int64_t p, int64_t tokens, const BcaShape& sh) {
+  if (dc == nullptr || !aligned16(dc)) return RDFFT_EINVAL;
+  if (overlaps(dc, sh.dc_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
+  if (tokens > 0) {
+    if (dx == nullptr || !aligned16(dx)) return RDFFT_EINVAL;
+    if (overlaps(x, sh.x_bytes, gy, sh.y_bytes)) return RDFFT_EINVAL;
+    if (overlaps(dx, sh.x_bytes, x, sh.x_bytes) || overlaps(dx, sh.x_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
+    if (dx == gy) {
+      if (d_in != d_out) return RDFFT_EINVAL;
+      if (p > 8192 && sh.q > rdfft::kMpMaxInPlaceBlocks) return RDFFT_EUNSUPPORTED;
+    } else if (overlaps(dx, sh.x_bytes, gy, sh.y_bytes)) {
+      return RDFFT_EINVAL;
+    }
+    if (overlaps(dc, sh.dc_bytes, x, sh.x_bytes) || overlaps(dc, sh.dc_bytes, gy, sh.y_bytes) ||
+        overlaps(dc, sh.dc_bytes, dx, sh.x_bytes))
+      return RDFFT_EINVAL;
+  }
+  return RDFFT_OK;
+}
+
+// Layers of a batch: nothing one layer writes may overlap anything of another layer (reads
+// may share buffers, e.g. one x for several layers).
+struct Span {
+  const void* p;
+  int64_t bytes;
+  bool written;
+};
+bool batch_disjoint(const std::vector<std::vector<Span>>& layers) {
+  for (size_t a = 0; a < layers.size(); ++a)
+    for (size_t b = a + 1; b < layers.size(); ++b)
+      for (const Span& u : layers[a])
+        for (const Span& v : layers[b])
+          if ((u.written || v.written) && overlaps(u.p, u.bytes, v.p, v.bytes)) return false;
+  return true;
+}
+
+constexpr int kMaxBatchCount = 1024;
+
 }  // namespace
 
 extern "C" {
@@ -188,13 +240,8 @@ int bca_forward(const void* x, const void* c_spectra, void* y, bca_grads_t* grad
   int st = check_bca(x, c_spectra, y, d_in, d_out, p, tokens, dtype, false, &sh);
   if (st != RDFFT_OK) return st;
   if (tokens == 0) return RDFFT_OK;
-  // y may be x itself (an in-place layer) only when the shapes agree
-  if (y == x) {
-    if (d_in != d_out) return RDFFT_EINVAL;
-    if (p > 8192 && sh.q > rdfft::kMpMaxInPlaceBlocks) return RDFFT_EUNSUPPORTED;
-  } else if (overlaps(x, sh.x_bytes, y, sh.y_bytes)) {
-    return RDFFT_EINVAL;
-  }
+  st = check_forward_alias(x, y, d_in, d_out, p, sh);
+  if (st != RDFFT_OK) return st;
   const float2* tw = nullptr;
   int num_cu = 0;
   st = ensure_device(&tw, &num_cu);
@@ -213,22 +260,8 @@ int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* gr
   if (st != RDFFT_OK) return st;
   float* dc = grads->dc;
   void* dx = grads->dx;
-  if (dc == nullptr || !aligned16(dc)) return RDFFT_EINVAL;
-  if (overlaps(dc, sh.dc_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
-  if (tokens > 0) {
-    if (dx == nullptr || !aligned16(dx)) return RDFFT_EINVAL;
-    if (overlaps(x, sh.x_bytes, gy, sh.y_bytes)) return RDFFT_EINVAL;
-    if (overlaps(dx, sh.x_bytes, x, sh.x_bytes) || overlaps(dx, sh.x_bytes, c_spectra, sh.c_bytes)) return RDFFT_EINVAL;
-    if (dx == gy) {
-      if (d_in != d_out) return RDFFT_EINVAL;
-      if (p > 8192 && sh.q > rdfft::kMpMaxInPlaceBlocks) return RDFFT_EUNSUPPORTED;
-    } else if (overlaps(dx, sh.x_bytes, gy, sh.y_bytes)) {
-      return RDFFT_EINVAL;
-    }
-    if (overlaps(dc, sh.dc_bytes, x, sh.x_bytes) || overlaps(dc, sh.dc_bytes, gy, sh.y_bytes) ||
-        overlaps(dc, sh.dc_bytes, dx, sh.x_bytes))
-      return RDFFT_EINVAL;
-  }
+  st = check_backward_grads(x, c_spectra, gy, dx, dc, d_in, d_out, p, tokens, sh);
+  if (st != RDFFT_OK) return st;
   const float2* tw = nullptr;
   int num_cu = 0;
   st = ensure_device(&tw, &num_cu);
@@ -237,6 +270,100 @@ int bca_backward(const void* x, const void* c_spectra, void* gy, bca_grads_t* gr
   return rdfft::launch_bca_backward(a, tw, reinterpret_cast<hipStream_t>(stream), num_cu) == hipSuccess
              ? RDFFT_OK
              : RDFFT_ELAUNCH;
+}
+
+int bca_forward_batched(int count, const void* const* x, const void* const* c_spectra, void* const* y, int64_t d_in,
+                        int64_t d_out, int64_t p, int64_t tokens, rdfft_dtype_t dtype, rdfft_stream_t stream) {
+  if (count < 0 || count > kMaxBatchCount) return RDFFT_EINVAL;
+  if (count == 0) return RDFFT_OK;
+  if (x == nullptr || c_spectra == nullptr || y == nullptr) return RDFFT_EINVAL;
+  BcaShape sh;
+  std::vector<std::vector<Span>> spans((size_t)count);
+  for (int b = 0; b < count; ++b) {
+    int st = check_bca(x[b], c_spectra[b], y[b], d_in, d_out, p, tokens, dtype, false, &sh);
+    if (st != RDFFT_OK) return st;
+    if (tokens > 0) {
+      st = check_forward_alias(x[b], y[b], d_in, d_out, p, sh);
+      if (st != RDFFT_OK) return st;
+    }
+    spans[b] = {{x[b], sh.x_bytes, false}, {c_spectra[b], sh.c_bytes, false}, {y[b], sh.y_bytes, true}};
+  }
+  if (tokens == 0) return RDFFT_OK;
+  if (!batch_disjoint(spans)) return RDFFT_EINVAL;
+  const float2* tw = nullptr;
+  int num_cu = 0;
+  int st = ensure_device(&tw, &num_cu);
+  if (st != RDFFT_OK) return st;
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (rdfft::bca_batch_fused(sh.logp, sh.q, sh.kb, dtype, false)) {
+    const rdfft::BcaArgs shape{nullptr, nullptr, nullptr, nullptr, nullptr, tokens, sh.q, sh.kb, sh.logp, dtype};
+    for (int b0 = 0; b0 < count; b0 += rdfft::kMaxBatch) {
+      rdfft::BcaBatch bt{};
+      bt.count = count - b0 < rdfft::kMaxBatch ? count - b0 : rdfft::kMaxBatch;
+      for (int i = 0; i < bt.count; ++i) {
+        bt.x[i] = x[b0 + i];
+        bt.c[i] = c_spectra[b0 + i];
+        bt.y[i] = y[b0 + i];
+      }
+      if (rdfft::launch_bca_forward_batched(shape, bt, tw, s, num_cu) != hipSuccess) return RDFFT_ELAUNCH;
+    }
+    return RDFFT_OK;
+  }
+  for (int b = 0; b < count; ++b) {
+    const rdfft::BcaArgs a{x[b], c_spectra[b], y[b], nullptr, nullptr, tokens, sh.q, sh.kb, sh.logp, dtype};
+    if (rdfft::launch_bca_forward(a, tw, s, num_cu) != hipSuccess) return RDFFT_ELAUNCH;
+  }
+  return RDFFT_OK;
+}
+
+int bca_backward_batched(int count, const void* const* x, const void* const* c_spectra, void* const* gy,
+                         const bca_grads_t* grads, int64_t d_in, int64_t d_out, int64_t p, int64_t tokens,
+                         rdfft_dtype_t dtype, rdfft_stream_t stream) {
+  if (count < 0 || count > kMaxBatchCount) return RDFFT_EINVAL;
+  if (count == 0) return RDFFT_OK;
+  if (x == nullptr || c_spectra == nullptr || gy == nullptr || grads == nullptr) return RDFFT_EINVAL;
+  BcaShape sh;
+  bool apart = true;  // every layer's dx apart from its gy
+  std::vector<std::vector<Span>> spans((size_t)count);
+  for (int b = 0; b < count; ++b) {
+    int st = check_bca(x[b], c_spectra[b], gy[b], d_in, d_out, p, tokens, dtype, true, &sh);
+    if (st != RDFFT_OK) return st;
+    st = check_backward_grads(x[b], c_spectra[b], gy[b], grads[b].dx, grads[b].dc, d_in, d_out, p, tokens, sh);
+    if (st != RDFFT_OK) return st;
+    apart = apart && grads[b].dx != gy[b];
+    spans[b] = {{x[b], sh.x_bytes, false},
+                {c_spectra[b], sh.c_bytes, false},
+                {gy[b], sh.y_bytes, true},
+                {grads[b].dx, tokens > 0 ? sh.x_bytes : 0, true},
+                {grads[b].dc, sh.dc_bytes, true}};
+  }
+  if (!batch_disjoint(spans)) return RDFFT_EINVAL;
+  const float2* tw = nullptr;
+  int num_cu = 0;
+  int st = ensure_device(&tw, &num_cu);
+  if (st != RDFFT_OK) return st;
+  const hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (tokens > 0 && apart && rdfft::bca_batch_fused(sh.logp, sh.q, sh.kb, dtype, true)) {
+    const rdfft::BcaArgs shape{nullptr, nullptr, nullptr, nullptr, nullptr, tokens, sh.q, sh.kb, sh.logp, dtype};
+    for (int b0 = 0; b0 < count; b0 += rdfft::kMaxBatch) {
+      rdfft::BcaBatch bt{};
+      bt.count = count - b0 < rdfft::kMaxBatch ? count - b0 : rdfft::kMaxBatch;
+      for (int i = 0; i < bt.count; ++i) {
+        bt.x[i] = x[b0 + i];
+        bt.c[i] = c_spectra[b0 + i];
+        bt.y[i] = gy[b0 + i];
+        bt.dx[i] = grads[b0 + i].dx;
+        bt.dc[i] = grads[b0 + i].dc;
+      }
+      if (rdfft::launch_bca_backward_batched(shape, bt, tw, s, num_cu) != hipSuccess) return RDFFT_ELAUNCH;
+    }
+    return RDFFT_OK;
+  }
+  for (int b = 0; b < count; ++b) {
+    const rdfft::BcaArgs a{x[b], c_spectra[b], gy[b], grads[b].dx, grads[b].dc, tokens, sh.q, sh.kb, sh.logp, dtype};
+    if (rdfft::launch_bca_backward(a, tw, s, num_cu) != hipSuccess) return RDFFT_ELAUNCH;
+  }
+  return RDFFT_OK;
 }
 
 int rdfft_init(void) {

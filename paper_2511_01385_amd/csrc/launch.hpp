@@ -55,6 +55,26 @@ struct BcaArgs {
 };
 
 hipError_t launch_bca_forward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu);
+
+// Independent layers of one shape (bca_forward_batched / bca_backward_batched): up to
+// kMaxBatch of them per launch, layer b of a launch in grid row blockIdx.y.
+constexpr int kMaxBatch = 32;
+struct BcaBatch {
+  int count;
+  const void* x[kMaxBatch];
+  const void* c[kMaxBatch];
+  void* y[kMaxBatch];  // forward output, or backward upstream gradient gy
+  void* dx[kMaxBatch];
+  float* dc[kMaxBatch];
+};
+// whether layers of this shape run in one grid per launch (the wave kernels' square layers;
+// the backward only with dx apart from gy); other batches run layer by layer
+bool bca_batch_fused(int logp, int q, int kb, int storage, bool backward);
+// shape: BcaArgs whose pointers are unused; the backward zeroes and fills every dc
+hipError_t launch_bca_forward_batched(const BcaArgs& shape, const BcaBatch& b, const float2* tw, hipStream_t stream,
+                                      int num_cu);
+hipError_t launch_bca_backward_batched(const BcaArgs& shape, const BcaBatch& b, const float2* tw, hipStream_t stream,
+                                       int num_cu);
 // also zeroes dc first and transforms it to the time domain afterwards
 hipError_t launch_bca_backward(const BcaArgs& a, const float2* tw, hipStream_t stream, int num_cu);
 

@@ -167,6 +167,42 @@ def test_bca_backward_long_blocks_in_place_at_most_eight_blocks(lib):
     assert lib.bca_backward(A, B, G, _grads(G, DC), 147456, 147456, 16384, 8, F32, None) == EUNSUP
 
 
+def _ptrs(*addrs):
+    return (ctypes.c_void_p * len(addrs))(*addrs)
+
+
+def test_bca_batched_validation(lib):
+    """Batched layers: the count, every layer's own checks, and no layer writing where another
+    layer reads or writes; these are refused before any device work (valid batches reach the
+    device check, which fails without a GPU)."""
+    d, p, t = 256, 64, 8
+    MB = 1 << 24  # well apart
+    xs, cs = _ptrs(A, A + MB), _ptrs(B, B)  # the layers may share their spectra
+    assert lib.bca_forward_batched(-1, xs, cs, xs, d, d, p, t, F32, None) == EINVAL
+    assert lib.bca_forward_batched(1025, xs, cs, xs, d, d, p, t, F32, None) == EINVAL
+    assert lib.bca_forward_batched(0, None, None, None, d, d, p, t, F32, None) == OK
+    ys = _ptrs(G, G + 64)  # the two outputs overlap
+    assert lib.bca_forward_batched(2, xs, cs, ys, d, d, p, t, F32, None) == EINVAL
+    ys = _ptrs(G, A + MB)  # layer 1 writes layer 1's own input (in place) - allowed
+    assert lib.bca_forward_batched(2, xs, cs, ys, d, d, p, t, F32, None) == _lib.RDFFT_EDEVICE
+    ys = _ptrs(A + MB, G)  # layer 0 writes layer 1's input
+    assert lib.bca_forward_batched(2, xs, cs, ys, d, d, p, t, F32, None) == EINVAL
+    ys = _ptrs(G, G + MB)
+    assert lib.bca_forward_batched(2, _ptrs(A, A), cs, ys, d, d, p, t, F32, None) == _lib.RDFFT_EDEVICE  # shared x
+    assert lib.bca_forward_batched(2, xs, cs, _ptrs(G, G + MB + 4), d, d, p, t, F32, None) == EINVAL  # misaligned
+    dx0, dc0 = A + (5 << 29), A + (6 << 29)  # apart from x, the spectra and gy
+    grads = (_lib.BcaGrads * 2)(_lib.BcaGrads(dx0, dc0), _lib.BcaGrads(dx0 + MB, dc0 + MB))
+    gys = _ptrs(G, G + MB)
+    assert lib.bca_backward_batched(2, xs, cs, gys, grads, d, d, p, t, F32, None) == _lib.RDFFT_EDEVICE
+    grads = (_lib.BcaGrads * 2)(_lib.BcaGrads(dx0, dc0), _lib.BcaGrads(dx0 + MB, dc0))  # one dc for both
+    assert lib.bca_backward_batched(2, xs, cs, gys, grads, d, d, p, t, F32, None) == EINVAL
+    grads = (_lib.BcaGrads * 2)(_lib.BcaGrads(dx0, dc0), _lib.BcaGrads(A, dc0 + MB))  # dx over layer 0's x
+    assert lib.bca_backward_batched(2, xs, cs, gys, grads, d, d, p, t, F32, None) == EINVAL
+    grads = (_lib.BcaGrads * 2)(_lib.BcaGrads(G, dc0), _lib.BcaGrads(G + MB, dc0 + MB))  # dx over gy: allowed
+    assert lib.bca_backward_batched(2, xs, cs, gys, grads, d, d, p, t, F32, None) == _lib.RDFFT_EDEVICE
+    assert lib.bca_backward_batched(2, xs, cs, gys, None, d, d, p, t, F32, None) == EINVAL
+
+
 def test_bca_backward_needs_grads(lib):
     assert lib.bca_backward(A, B, G, None, 256, 256, 64, 8, F32, None) == EINVAL
 
