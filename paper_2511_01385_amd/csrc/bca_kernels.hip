@@ -166,6 +166,8 @@ hipError_t launch_bca_backward_batched(const BcaArgs& a, const BcaBatch& b, cons
                                        int num_cu) {
   if (!bca_batch_fused(a.logp, a.q, a.kb, a.storage, true) || b.count < 1 || b.count > kMaxBatch || a.tokens < 1)
     return hipErrorInvalidValue;
+  for (int i = 0; i < b.count; ++i)
+    if (b.dx[i] == b.y[i]) return hipErrorInvalidValue;
   return store_tables(a.storage).wave_bwd_batched[a.q - 1][a.logp - 1](a, b, tw, stream, num_cu);
 }
 
