@@ -697,9 +697,17 @@ constexpr int kSqMaxSlots = 16;  // C and dC values per thread: bins per thread 
 // Tokens per tile of the square-layer kernels: the largest TT (at most 64 and the token
 // count) whose TT*rpt spectra, plus a spare region when TT*QB transforms leave some of
 // the ng row groups idle, fit in `budget` bytes.  0 when one token does not fit.
-static int sq_tokens_per_tile(int logn, int rpt, int qb, int ng, int64_t tokens, int64_t budget, bool* spare) {
+// Tokens per tile of the square-layer kernels: the most whose regions fit `budget`, at most
+// 64, and (spread > 0) at most tokens / spread, so that a short batch still reaches `spread`
+// workgroups.  The forward spreads over the CUs (the 256-wide layer's 128 tokens: 2 tiles of 64,
+// 7.5 us; 128 tiles of 1, 4.0 us); the backward does not, since every workgroup adds a dC
+// partial sum (1024-wide, 512 tokens: 31 us as is, 40 us spread).
+static int sq_tokens_per_tile(int logn, int rpt, int qb, int ng, int64_t tokens, int64_t budget, bool* spare,
+                              int spread = 0) {
   const int64_t rb = region_bytes(logn);
-  for (int tt = (int)std::min<int64_t>(64, std::max<int64_t>(tokens, 1)); tt >= 1; --tt) {
+  int64_t top = std::min<int64_t>(64, std::max<int64_t>(tokens, 1));
+  if (spread > 0) top = std::min<int64_t>(top, std::max<int64_t>(1, (tokens + spread - 1) / spread));
+  for (int tt = (int)top; tt >= 1; --tt) {
     const bool sp = (tt * qb) % ng != 0;
     if ((tt * rpt + (sp ? 1 : 0)) * rb <= budget) {
       *spare = sp;
@@ -723,8 +731,8 @@ static hipError_t fwd_sq_impl(const BcaArgs& a, const float2* tw, hipStream_t st
   constexpr int ng = WG / BcaPlan<LOGN>::TPR;
   // two workgroups per CU, or one when a token's spectra need more than half the LDS
   bool spare = false;
-  int TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit / 2, &spare);
-  if (TT == 0) TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit, &spare);
+  int TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit / 2, &spare, num_cu);
+  if (TT == 0) TT = sq_tokens_per_tile(LOGN, rpt, QB, ng, a.tokens, kLdsLimit, &spare, num_cu);
   if (TT == 0) return hipErrorInvalidValue;
   const size_t lds = (size_t)(TT * rpt + (spare ? 1 : 0)) * region_bytes(LOGN);
   static const hipError_t attr = set_lds_limit(bca_forward_sq_kernel<LOGN, St, QB>);
