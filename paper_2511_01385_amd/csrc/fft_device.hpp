@@ -127,42 +127,92 @@ struct Dft<4, INV> {
   }
 };
 
-// R = R1 * R2 by one decimation-in-time step: n = R2*n1 + n2, k = k1 + R1*k2.
-template <int R1, int R2, bool INV>
-__device__ __forceinline__ void dft_split(float2* v) {
-  constexpr int R = R1 * R2;
-  float2 t[R];
-  static_for<R2>([&](auto n2c) {
-    constexpr int n2 = decltype(n2c)::value;
-    float2 u[R1];
-    static_for<R1>([&](auto n1c) { u[decltype(n1c)::value] = v[R2 * decltype(n1c)::value + n2]; });
-    Dft<R1, INV>::run(u);
-    static_for<R1>([&](auto k1c) {
-      constexpr int k1 = decltype(k1c)::value;
-      t[k1 * R2 + n2] = rot<R, n2 * k1, INV>(u[k1]);
-    });
-  });
-  static_for<R1>([&](auto k1c) {
-    constexpr int k1 = decltype(k1c)::value;
-    Dft<R2, INV>::run(&t[k1 * R2]);
-    static_for<R2>([&](auto k2c) {
-      constexpr int k2 = decltype(k2c)::value;
-      v[k1 + R1 * k2] = t[k1 * R2 + k2];
-    });
-  });
+// a <- a + W b and b <- a - W b for the constant W = W_M^J (exp(-2 pi i J / M), its
+// conjugate when INV).  W is written as (-i)^q cos(phi) (1 - i tan(phi)) with |phi| <= pi/4:
+// the factor (1 - i tan(phi)) costs two FMAs, (-i)^q only swaps and negates, and cos(phi)
+// rides in the FMAs of the sum and difference, so a butterfly costs six instructions
+// (four when phi = 0) instead of a complex multiply plus an add and a subtract.
+template <int M, int J, bool INV>
+__device__ __forceinline__ void bfly2(float2& a, float2& b) {
+  static_assert(64 % M == 0, "constant rotations need M | 64");
+  constexpr int j = ((J % M) + M) % M * (64 / M);  // the angle in units of 2 pi / 64
+  constexpr int q = ((j + 8) / 16) % 4;              // nearest quarter turn
+  constexpr int phi = j - 16 * ((j + 8) / 16);       // the rest, in [-8, 8)
+  float2 e = b;
+  if constexpr (phi != 0) {
+    constexpr float t = (float)(sin64(phi) / cos64(phi));
+    // (1 -+ i t) b
+    e = INV ? make_float2(fmaf(-t, b.y, b.x), fmaf(t, b.x, b.y)) : make_float2(fmaf(t, b.y, b.x), fmaf(-t, b.x, b.y));
+  }
+  // (-i)^q e, or i^q e for the inverse
+  constexpr int qq = INV ? (4 - q) % 4 : q;
+  if constexpr (qq == 1) e = make_float2(e.y, -e.x);
+  else if constexpr (qq == 2) e = make_float2(-e.x, -e.y);
+  else if constexpr (qq == 3) e = make_float2(-e.y, e.x);
+  if constexpr (phi == 0) {
+    const float2 s = c_add(a, e), d = c_sub(a, e);
+    a = s;
+    b = d;
+  } else {
+    constexpr float c = (float)cos64(phi);
+    const float2 s = make_float2(fmaf(c, e.x, a.x), fmaf(c, e.y, a.y));
+    const float2 d = make_float2(fmaf(-c, e.x, a.x), fmaf(-c, e.y, a.y));
+    a = s;
+    b = d;
+  }
 }
 
-template <bool INV>
-struct Dft<8, INV> {
-  __device__ __forceinline__ static void run(float2* v) { dft_split<4, 2, INV>(v); }
+// DFT of R points of the inputs W_M^{nJ} x[n] (conjugate rotations when INV), natural order
+// in and out, by radix-2 decimation in time: the even and odd halves are DFTs of the same
+// form with 2J, and output k pairs with k + R/2 through the constant W_R^k W_M^J = W_M^{J + kM/R}.
+template <int R, int M, int J, bool INV>
+struct TwDft {
+  __device__ __forceinline__ static void run(float2* x) {
+    float2 e[R / 2], o[R / 2];
+    static_for<R / 2>([&](auto mc) {
+      constexpr int m = decltype(mc)::value;
+      e[m] = x[2 * m];
+      o[m] = x[2 * m + 1];
+    });
+    TwDft<R / 2, M, 2 * J, INV>::run(e);
+    TwDft<R / 2, M, 2 * J, INV>::run(o);
+    static_for<R / 2>([&](auto kc) {
+      constexpr int k = decltype(kc)::value;
+      bfly2<M, J + k * (M / R), INV>(e[k], o[k]);
+      x[k] = e[k];
+      x[k + R / 2] = o[k];
+    });
+  }
 };
-template <bool INV>
-struct Dft<16, INV> {
-  __device__ __forceinline__ static void run(float2* v) { dft_split<4, 4, INV>(v); }
+template <int M, int J, bool INV>
+struct TwDft<1, M, J, INV> {
+  __device__ __forceinline__ static void run(float2*) {}
 };
+
+template <bool INV>
+struct Dft<8, INV> : TwDft<8, 8, 0, INV> {};
+template <bool INV>
+struct Dft<16, INV> : TwDft<16, 16, 0, INV> {};
+// R = 32 as 8 DFTs of 4 points over stride-8 inputs, then 4 rotated DFTs of 8 points
+// (n = 8 n1 + n2, k = k1 + 4 k2): the same instruction count as the radix-2 recursion,
+// with shorter live ranges at a thread's 128-register limit.
 template <bool INV>
 struct Dft<32, INV> {
-  __device__ __forceinline__ static void run(float2* v) { dft_split<4, 8, INV>(v); }
+  __device__ __forceinline__ static void run(float2* v) {
+    float2 u[8][4];
+    static_for<8>([&](auto n2c) {
+      constexpr int n2 = decltype(n2c)::value;
+      static_for<4>([&](auto n1c) { u[n2][decltype(n1c)::value] = v[8 * decltype(n1c)::value + n2]; });
+      Dft<4, INV>::run(u[n2]);
+    });
+    static_for<4>([&](auto k1c) {
+      constexpr int k1 = decltype(k1c)::value;
+      float2 w[8];
+      static_for<8>([&](auto n2c) { w[decltype(n2c)::value] = u[decltype(n2c)::value][k1]; });
+      TwDft<8, 32, k1, INV>::run(w);
+      static_for<8>([&](auto k2c) { v[k1 + 4 * decltype(k2c)::value] = w[decltype(k2c)::value]; });
+    });
+  }
 };
 
 // ----------------------------------------------------------------------------------
