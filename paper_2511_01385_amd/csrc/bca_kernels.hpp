@@ -1152,6 +1152,9 @@ static hipError_t bwd_wave_launch(const WavePtrs<St, MAXB>& ptrs, int count, boo
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (staged) {
+    if (count == 1)
+      return launch_dc_finish(reinterpret_cast<const float2*>(ptrs.y[0]), ptrs.dc[0], QB * QB, LOGN, QKN, (int)grid,
+                              region_f2, tw, stream);
     FinishPtrs<kMaxBatch> f{};
     for (int b = 0; b < count; ++b) {
       f.stage[b] = reinterpret_cast<const float2*>(ptrs.y[b]);
