@@ -421,8 +421,9 @@ struct RowPlan {
   static constexpr int TPR = N / E;                       // threads per row
   static constexpr int RW = TPR >= 256 ? 1 : 256 / TPR;   // rows per 256-thread workgroup
   static constexpr int WG = TPR * RW;
-  // LDS float2 per row: one exchange chunk, or the half-spectrum partner exchange
-  static constexpr int LDS_F2 = TPR == 1 ? 0 : lds_padded_size(N / C > N / 2 ? N / C : N / 2);
+  // LDS float2 per row: one exchange chunk, or the half-spectrum partner exchange, at a
+  // stride that keeps the rows of one wavefront on different banks
+  static constexpr int LDS_F2 = TPR == 1 ? 0 : lds_row_stride(N / C > N / 2 ? N / C : N / 2, TPR);
   static_assert(plan_is_consistent(LOGN), "inconsistent plan");
 
 };

@@ -115,4 +115,12 @@ constexpr int kTableEntries = plan_table_offset(kMaxLogN + 1);  // float2 entrie
 constexpr int lds_pad(int i) { return i + (i >> 4); }
 constexpr int lds_padded_size(int count) { return count + (count >> 4) + 1; }
 
+// Stride between the LDS regions of rows that share a wavefront.  ds_write_b64 and the
+// paired ds_read2_b64 serve 16 lanes per cycle from 32 four-byte banks, so the 16/TPR rows
+// in such a group should fall on disjoint banks: one row's lanes cover 2*TPR words, which
+// asks for a stride of TPR float2 modulo 16.  Rows of 16 or more threads need nothing.
+constexpr int lds_row_stride(int count, int tpr) {
+  return tpr >= 16 ? lds_padded_size(count) : lds_padded_size(count) + ((tpr - lds_padded_size(count) % 16) % 16 + 16) % 16;
+}
+
 }  // namespace rdfft
