@@ -274,11 +274,15 @@ struct BcaSqFwd {
   static constexpr int TS = TB / TJ;                                        // token phases
   static constexpr int IPT = QB / TJ;                                       // output blocks per thread
   static constexpr int NSL = IPT * QB;
+  // the 512-bin layers (p = 1024) run two 512-thread workgroups per CU, four waves per SIMD,
+  // which leaves a wave 128 VGPRs: ask the compiler to stay within them
+  static constexpr int MIN_WAVES = (WG == 512 && N == 512) ? 4 : 1;
 };
 constexpr int kFwdSqWG = 512;
 
 template <int LOGN, class St, int QB, int WG = kFwdSqWG>
-__global__ void __launch_bounds__(WG) bca_forward_sq_kernel(const ElemOf<St>* x, const ElemOf<St>* __restrict__ c,
+__global__ void __launch_bounds__(WG) __attribute__((amdgpu_waves_per_eu(BcaSqFwd<LOGN, QB, WG>::MIN_WAVES)))
+bca_forward_sq_kernel(const ElemOf<St>* x, const ElemOf<St>* __restrict__ c,
                                                                      ElemOf<St>* y, int64_t tokens, int tt_per_tile,
                                                                      int64_t ntiles, const float2* __restrict__ tw) {
   using B = BcaPlan<LOGN>;

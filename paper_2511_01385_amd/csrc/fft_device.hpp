@@ -423,7 +423,9 @@ struct RowPlan {
   static constexpr int WG = TPR * RW;
   // LDS float2 per row: one exchange chunk, or the half-spectrum partner exchange, at a
   // stride that keeps the rows of one wavefront on different banks
-  static constexpr int LDS_F2 = TPR == 1 ? 0 : lds_row_stride(N / C > N / 2 ? N / C : N / 2, TPR);
+  static constexpr int LDS_F2_STD = TPR == 1 ? 0 : lds_row_stride(N / C > N / 2 ? N / C : N / 2, TPR);
+  static constexpr int LDS_F2_WIDE = plan_has_wide_exchange(LOGN, CH) ? lds_pad_wide(N - 1) + 1 : 0;
+  static constexpr int LDS_F2 = LDS_F2_STD > LDS_F2_WIDE ? LDS_F2_STD : LDS_F2_WIDE;
   static_assert(plan_is_consistent(LOGN), "inconsistent plan");
 
 };
@@ -507,6 +509,9 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
   constexpr int R2 = radix(LOGN, Q + 1), BPT2 = E / R2;
   constexpr int CS = N / C;  // slots per chunk
   static_assert(C == 1 || ((BPT % C == 0 || BPT == 1) && R2 % C == 0), "chunking needs C | BPT (or BPT = 1) and C | R'");
+  // every address of this exchange goes through one padding rule, the wide one where it applies
+  constexpr bool WIDE = wide_exchange(LOGN, Q, C);
+  const auto xp = [](int i) { return WIDE ? lds_pad_wide(i) : lds_pad(i); };
   float2 nv[E];
   static_for<C>([&](auto cc) {
     constexpr int c = decltype(cc)::value;
@@ -515,10 +520,10 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
       auto write = [&]() {
         const int g = t + b * TPR;
         const int k = g & (Ns - 1);
-        const int pb = lds_pad((g - k) * R + k - c * CS);
+        const int pb = xp((g - k) * R + k - c * CS);
         static_for<R>([&](auto rc) {
           constexpr int r = decltype(rc)::value;
-          lds[pb + pad_step(r * Ns)] = v[b * R + r];
+          lds[pb + xp(r * Ns)] = v[b * R + r];
         });
       };
       if constexpr (BPT % C == 0) {
@@ -530,11 +535,11 @@ __device__ __forceinline__ void stockham_exchange(float2* v, int t, float2* lds)
     row_sync<TPR>();
     static_for<BPT2>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
-      const int pg = lds_pad(bfly<LOGN, Q + 1, MIR>(t, b));
+      const int pg = xp(bfly<LOGN, Q + 1, MIR>(t, b));
       static_for<R2>([&](auto rc) {
         constexpr int r = decltype(rc)::value;
         // chunk c starts at r = c*R2/C, i.e. at index c*CS: the address is g + (r - c*R2/C)*(N/R2)
-        if constexpr (r / (R2 / C) == c) nv[b * R2 + r] = lds[pg + pad_step((r - c * (R2 / C)) * (N / R2))];
+        if constexpr (r / (R2 / C) == c) nv[b * R2 + r] = lds[pg + xp((r - c * (R2 / C)) * (N / R2))];
       });
     });
     row_sync<TPR>();

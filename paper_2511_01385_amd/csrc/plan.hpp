@@ -115,6 +115,23 @@ constexpr int kTableEntries = plan_table_offset(kMaxLogN + 1);  // float2 entrie
 constexpr int lds_pad(int i) { return i + (i >> 4); }
 constexpr int lds_padded_size(int count) { return count + (count >> 4) + 1; }
 
+// The exchange after a radix-8 pass of stride 8 (the n = 1024 plan 8.8.8) writes groups of 8
+// consecutive slots 64 apart, and lds_pad puts neighbouring groups on overlapping banks (one
+// extra cycle per 16 lanes).  Four more slots of padding every 64 move every other group by
+// half the banks.  That padding stays additive over the exchange's base-plus-offset addresses
+// (write bases 64m + j with j < 8 and offsets below 64; read offsets multiples of 64) whenever
+// the next pass's sub-transform stride N/R' is a multiple of 64, which the test requires.
+constexpr int lds_pad_wide(int i) { return i + (i >> 4) + 4 * (i >> 6); }
+constexpr bool wide_exchange(int logn, int q, int chunks) {
+  return chunks == 1 && q + 1 < num_passes(logn) && stride_before(logn, q) == 8 && radix(logn, q) == 8 &&
+         ((1 << logn) / radix(logn, q + 1)) % 64 == 0;
+}
+constexpr bool plan_has_wide_exchange(int logn, int chunks) {
+  bool any = false;
+  for (int q = 0; q + 1 < num_passes(logn); ++q) any = any || wide_exchange(logn, q, chunks);
+  return any;
+}
+
 // Stride between the LDS regions of rows that share a wavefront.  ds_write_b64 and the
 // paired ds_read2_b64 serve 16 lanes per cycle from 32 four-byte banks, so the 16/TPR rows
 // in such a group should fall on disjoint banks: one row's lanes cover 2*TPR words, which
