@@ -427,6 +427,7 @@ struct RowPlan {
   static constexpr int LDS_F2_WIDE = plan_has_wide_exchange(LOGN, CH) ? lds_pad_wide(N - 1) + 1 : 0;
   static constexpr int LDS_F2 = LDS_F2_STD > LDS_F2_WIDE ? LDS_F2_STD : LDS_F2_WIDE;
   static_assert(plan_is_consistent(LOGN), "inconsistent plan");
+  static_assert(exchange_split_ok(LOGN, CH), "an exchange's split LDS addresses differ from the padded index");
 
 };
 

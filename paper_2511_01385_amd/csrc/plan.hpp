@@ -132,6 +132,47 @@ constexpr bool plan_has_wide_exchange(int logn, int chunks) {
   return any;
 }
 
+// The exchanges address LDS as pad(base) + pad(offset): a per-butterfly base and compile-time
+// offsets.  pad(base + offset) - pad(base) - pad(offset) is the carry out of the low four
+// bits (plus four times the carry out of the low six for lds_pad_wide), so the split is exact
+// when (base & 15) + (offset & 15) < 16 (and (base & 63) + (offset & 63) < 64) for every pair.
+// exchange_split_ok checks that for every exchange of a plan, over all residues of the bases
+// mod 64 and the largest low bits of the offsets, so a plan or padding that breaks it does not
+// compile.  (The post-pass and pre-pass partner exchanges take the split form only when their
+// offsets are multiples of 16, which carry nothing.)
+constexpr bool split_carry_free(int base, int off_low4, int off_low6, bool wide) {
+  return (base & 15) + off_low4 < 16 && (!wide || (base & 63) + off_low6 < 64);
+}
+constexpr bool exchange_split_ok(int logn, int chunks) {
+  if (logn == 0) return true;
+  const int N = 1 << logn, NP = num_passes(logn), CS = N / chunks;
+  if (chunks > 1 && CS % 64 != 0) return false;  // a chunk's origin must leave the low bits alone
+  for (int q = 0; q + 1 < NP; ++q) {
+    const int R = radix(logn, q), Ns = stride_before(logn, q), R2 = radix(logn, q + 1);
+    const bool wide = wide_exchange(logn, q, chunks);
+    // writes: base (g - k) R + k - c CS, offsets r Ns (r < R)
+    int l4 = 0, l6 = 0;
+    for (int r = 0; r < R; ++r) {
+      l4 = (r * Ns) % 16 > l4 ? (r * Ns) % 16 : l4;
+      l6 = (r * Ns) % 64 > l6 ? (r * Ns) % 64 : l6;
+    }
+    const int nm = N / (R * Ns) < 64 ? N / (R * Ns) : 64, nk = Ns < 64 ? Ns : 64;
+    for (int m = 0; m < nm; ++m)
+      for (int k = 0; k < nk; ++k)
+        if (!split_carry_free((Ns * R * m + k) % 64, l4, l6, wide)) return false;
+    // reads: base g < N/R', offsets j N/R' (j < R'/chunks)
+    l4 = 0, l6 = 0;
+    for (int j = 0; j < R2 / chunks; ++j) {
+      l4 = (j * (N / R2)) % 16 > l4 ? (j * (N / R2)) % 16 : l4;
+      l6 = (j * (N / R2)) % 64 > l6 ? (j * (N / R2)) % 64 : l6;
+    }
+    const int ng = N / R2 < 64 ? N / R2 : 64;
+    for (int g = 0; g < ng; ++g)
+      if (!split_carry_free(g, l4, l6, wide)) return false;
+  }
+  return true;
+}
+
 // Stride between the LDS regions of rows that share a wavefront.  ds_write_b64 and the
 // paired ds_read2_b64 serve 16 lanes per cycle from 32 four-byte banks, so the 16/TPR rows
 // in such a group should fall on disjoint banks: one row's lanes cover 2*TPR words, which
