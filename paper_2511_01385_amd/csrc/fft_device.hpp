@@ -294,6 +294,22 @@ struct ConstF16 {
   __device__ __forceinline__ float2 load(int m) const { return f16x2_to_f32(base[m]); }
 };
 
+// The accessor moved by g slots, for the accessors that are plain pointers: a butterfly's
+// loads and stores then take one address each and compile-time offsets that the memory
+// instructions carry as immediates.  Other accessors (LDS, halfcomplex) index as before.
+template <class A>
+struct PlainPointer : std::false_type {};
+template <> struct PlainPointer<GlobalF32> : std::true_type {};
+template <> struct PlainPointer<GlobalBF16> : std::true_type {};
+template <> struct PlainPointer<GlobalF16> : std::true_type {};
+template <> struct PlainPointer<ConstF32> : std::true_type {};
+template <> struct PlainPointer<ConstBF16> : std::true_type {};
+template <> struct PlainPointer<ConstF16> : std::true_type {};
+// ... used by plans with at most 16 values per thread: the 32-value plan (n = 65536) is at its
+// register limit and spills with the extra live addresses
+template <class A, int LOGN>
+constexpr bool shifted_access() { return PlainPointer<A>::value && kElems[LOGN] <= 16; }
+
 // A row's packed spectrum in the halfcomplex layout (Sec. 4.1, Memory Layout): Re Y_k at
 // real slot k (0 <= k <= N) and Im Y_k at real slot 2N - k (1 <= k < N).  Pair slot m of the
 // pairs layout is thus the two real slots (m, 2N - m), and pair slot 0 = (Y_0, Y_{n/2}) the
@@ -579,10 +595,18 @@ __device__ __forceinline__ void load_forward(int t, const Src& src, typename Src
     static_for<BPT0>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * TPR;
-      static_for<R0>([&](auto rc) {
-        constexpr int r = decltype(rc)::value;
-        raw[b * R0 + r] = src.load_raw(g + r * (N / R0));
-      });
+      if constexpr (shifted_access<Src, LOGN>()) {
+        const auto* p = src.base + g;
+        static_for<R0>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          raw[b * R0 + r] = p[r * (N / R0)];
+        });
+      } else {
+        static_for<R0>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          raw[b * R0 + r] = src.load_raw(g + r * (N / R0));
+        });
+      }
     });
   }
 }
@@ -648,8 +672,19 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
           hi = z ? zh : hi;
           hi_idx = z ? N / 2 : hi_idx;
         }
-        dst.store(k, lo);
-        dst.store(hi_idx, hi);
+        if constexpr (shifted_access<Dst, LOGN>()) {
+          // bins k = kb + j N/RL from kb's address, partners N - k from N - kb's (thread
+          // 0's first partner is slot N/2)
+          constexpr int jj = j < RL / 2 ? j : j - RL / 2;
+          auto* lo_p = dst.base + (j < RL / 2 ? t : kb1 + (RL / 2) * NsL);
+          auto* hi_p = dst.base + (N - (j < RL / 2 ? t : kb1 + (RL / 2) * NsL));
+          lo_p[jj * NsL] = Dst::narrow(lo);
+          if constexpr (j == 0) (z ? dst.base + N / 2 : hi_p)[0] = Dst::narrow(hi);
+          else hi_p[-jj * NsL] = Dst::narrow(hi);
+        } else {
+          dst.store(k, lo);
+          dst.store(hi_idx, hi);
+        }
       });
       return;
     }
@@ -727,6 +762,14 @@ __device__ __forceinline__ void row_forward_loaded(int t, bool active, const typ
           // k = t + TPR*(b + BPL*r): register index j = b + BPL*r
           dst.lo[b + BPL * r] = lo;
           dst.hi[b + BPL * r] = hi;
+        } else if constexpr (shifted_access<Dst, LOGN>()) {
+          // bins g + r N/RL from g's address, partners N - g - r N/RL from N - g's (thread
+          // 0's first partner is slot N/2)
+          auto* lo_p = dst.base + g;
+          auto* hi_p = dst.base + (N - g);
+          lo_p[r * NsL] = Dst::narrow(lo);
+          if constexpr (b == 0 && r == 0) (t == 0 ? dst.base + N / 2 : hi_p)[0] = Dst::narrow(hi);
+          else hi_p[-r * NsL] = Dst::narrow(hi);
         } else {
           dst.store(k, lo);
           dst.store(hi_idx, hi);
@@ -763,14 +806,27 @@ __device__ __forceinline__ void load_inverse(int t, const Src& src, typename Src
     static_for<BPT0>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * TPR;
-      static_for<R0 / 2>([&](auto rc) {
-        constexpr int r = decltype(rc)::value;
-        const int m = g + r * (N / R0);
-        // m == 0 only for thread 0 at (b, r) = (0, 0); it pairs with slot N/2 instead of N
-        const bool z = (b == 0 && r == 0) ? (t == 0) : false;
-        raw[b * R0 + r] = src.load_raw(m);
-        raw[b * R0 + R0 / 2 + r] = src.load_raw(z ? N / 2 : N - m);
-      });
+      if constexpr (shifted_access<Src, LOGN>()) {
+        // slots g + r S0 from one address, partners N - g - r S0 from another (thread 0's
+        // first partner is slot N/2)
+        const auto* lo = src.base + g;
+        const auto* hi = src.base + (N - g);
+        static_for<R0 / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          raw[b * R0 + r] = lo[r * (N / R0)];
+          if constexpr (b == 0 && r == 0) raw[b * R0 + R0 / 2 + r] = (t == 0 ? src.base + N / 2 : hi)[0];
+          else raw[b * R0 + R0 / 2 + r] = hi[-r * (N / R0)];
+        });
+      } else {
+        static_for<R0 / 2>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          const int m = g + r * (N / R0);
+          // m == 0 only for thread 0 at (b, r) = (0, 0); it pairs with slot N/2 instead of N
+          const bool z = (b == 0 && r == 0) ? (t == 0) : false;
+          raw[b * R0 + r] = src.load_raw(m);
+          raw[b * R0 + R0 / 2 + r] = src.load_raw(z ? N / 2 : N - m);
+        });
+      }
     });
   }
 }
@@ -868,10 +924,18 @@ __device__ __forceinline__ void row_inverse_loaded(int t, bool active, const typ
     static_for<BPL>([&](auto bc) {
       constexpr int b = decltype(bc)::value;
       const int g = t + b * TPR;
-      static_for<RL>([&](auto rc) {
-        constexpr int r = decltype(rc)::value;
-        dst.store(g + r * NsL, v[b * RL + r]);
-      });
+      if constexpr (shifted_access<Dst, LOGN>()) {
+        auto* p = dst.base + g;
+        static_for<RL>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          p[r * NsL] = Dst::narrow(v[b * RL + r]);
+        });
+      } else {
+        static_for<RL>([&](auto rc) {
+          constexpr int r = decltype(rc)::value;
+          dst.store(g + r * NsL, v[b * RL + r]);
+        });
+      }
     });
   }
 }
